@@ -1,0 +1,285 @@
+"""Throughput of the FoE per-cluster MoE block on one MI355X.
+
+One step = one foe_cluster_block call (route -> permute -> grouped SwiGLU FFN
+-> combine for every cluster, then the local reduction) on synthetic inputs
+already resident in HBM.  Prints ONE JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config NAME]
+                  [--no-graph] [--cpu-seconds S]
+
+Default workload: the decode-shaped cluster block (T=128, d=2048, E=16, k=2,
+F=1024, bf16).  Several independent weight/input sets are rotated so the
+working set exceeds the 256 MB Infinity Cache.
+
+Timed passes (both over K steps, HIP events on the library's stream):
+  A  plain steps -> value / ms_per_step (replayed from HIP graphs unless
+     --no-graph; the eager time is reported beside it)
+  B  the same steps with every kernel bracketed by HIP events (the library's
+     timing hooks) -> per-kernel average duration and the roofline object
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "tokens/s and expert-FFN TFLOP/s per FoE cluster block (decode & prefill), 1 GPU"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
+FP32_VALU_PEAK_TFLOPS = 157.3   # fp32 vector
+DEFAULT_CONFIG = "decode_bf16"
+MALL_BYTES = 256 << 20
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default=DEFAULT_CONFIG)
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="budget of the oracle CPU baseline (0 = skip)")
+    return ap.parse_args()
+
+
+def kernel_work(name, cfg, e_touched):
+    """Algorithmic (flops, bytes) of ONE launch of kernel `name` (one cluster)."""
+    T, d, E, k, F, C = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["F"], cfg["C"]
+    s = 2 if cfg["dtype"] == "bf16" else 4
+    R = T * k
+    if name == "route":
+        return 2.0 * T * d * E, T * d * s + E * d * s + 8.0 * R
+    if name == "permute_scatter":
+        return 0.0, T * d * s + R * d * s + 4.0 * R
+    if name in ("ffn_gateup", "ffn_gateup_f32"):
+        return 4.0 * R * d * F, 2.0 * e_touched * F * d * s + R * d * s + R * F * s
+    if name in ("ffn_down", "ffn_down_f32"):
+        return 2.0 * R * F * d, 1.0 * e_touched * d * F * s + R * F * s + R * d * s
+    if name == "combine":
+        direct = C == 1
+        return 2.0 * R * d, R * d * s + 8.0 * R + (2 if direct else 1) * T * d * s
+    if name == "reduce":
+        return 2.0 * C * T * d, (C + 2.0) * T * d * s
+    return 0.0, 0.0
+
+
+def roofline(name, cfg, e_touched, avg_s):
+    flops, nbytes = kernel_work(name, cfg, e_touched)
+    if cfg["dtype"] == "f32" and name.startswith("ffn"):
+        bound, peak, unit, achieved = "alu", FP32_VALU_PEAK_TFLOPS, "TFLOP/s", flops / avg_s / 1e12
+    elif nbytes > 0 and flops / nbytes > BF16_MFMA_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
+        bound, peak, unit, achieved = "mfma", BF16_MFMA_PEAK_TFLOPS, "TFLOP/s", flops / avg_s / 1e12
+    else:
+        bound, peak, unit, achieved = "hbm", HBM_PEAK_GBS, "GB/s", nbytes / avg_s / 1e9
+    return {"kernel": name, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
+            "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+            "avg_us": round(avg_s * 1e6, 3), "flops_per_launch": flops,
+            "bytes_per_launch": nbytes}
+
+
+def cpu_baseline(cfg_name, budget_s):
+    """The oracle as it stands, timed on this host's cores on a bounded sample."""
+    import numpy as np
+
+    import oracle
+    from paper_2605_06206_amd import synth
+
+    try:
+        from threadpoolctl import threadpool_info
+        pools = threadpool_info()
+        threads = max([p.get("num_threads", 1) for p in pools] or [1])
+        blas = ",".join(sorted({p.get("internal_api", "?") for p in pools}))
+    except Exception:  # pragma: no cover - informational only
+        threads, blas = os.cpu_count(), "unknown"
+    cfg = dict(synth.CONFIGS[cfg_name])
+    # a token prefix small enough for ~1 s per oracle call
+    per_tok = cfg["C"] * (cfg["k"] * 6.0 * cfg["d"] * cfg["F"] + 2.0 * cfg["d"] * cfg["E"])
+    T_s = int(max(16, min(cfg["T"], 2e9 / per_tok)))
+    inp = synth.make_block_inputs(cfg_name, T=T_s) if T_s < cfg["T"] else synth.make_block_inputs(cfg_name)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.cluster_block(inp["x"], inp["clusters"], cfg["k"])
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 1000:
+            break
+    tok_s = reps * T_s / el
+    return {"value": round(tok_s, 2), "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{reps} oracle runs (fp64 numpy) of the block on the first {T_s} of "
+                      f"{cfg['T']} tokens, {el:.1f} s, BLAS {blas}, "
+                      f"affinity {len(os.sched_getaffinity(0))} cpus"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: the per-cluster block has no multi-GPU path in "
+              "this build (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2605_06206_amd import foe, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    dev = "cuda:0"
+    cfg = dict(synth.CONFIGS[args.config], name=args.config)
+    dt = cfg["dtype"]
+    T, d, E, k, F, C = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["F"], cfg["C"]
+    s_el = 2 if dt == "bf16" else 4
+    set_bytes = C * (3 * E * F * d + E * d) * s_el + T * d * s_el
+    nsets = int(min(8, max(1, math.ceil(2 * MALL_BYTES / set_bytes))))
+
+    def up(a):
+        if dt == "bf16":
+            return torch.from_numpy(synth.bf16_bits(a)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+
+    sets = []
+    for i in range(nsets):
+        inp = synth.make_block_inputs(args.config, weight_set=i)
+        cls = inp["clusters"]
+        st = {"x": up(inp["x"])}
+        for key in ("w_router", "w_gate", "w_up", "w_down"):
+            st[key] = up(np.stack([c[key] for c in cls]))
+        st["bias"] = (torch.from_numpy(np.stack([c["bias"] for c in cls])).to(dev)
+                      if cls[0]["bias"] is not None else None)
+        sets.append(st)
+        del inp, cls
+
+    L = foe.lib()
+    dtc = foe.BF16 if dt == "bf16" else foe.F32
+    ws_n = foe.workspace_bytes("cluster_block", dtc, C, T, d, E, k, F)
+    ws = torch.empty(ws_n, dtype=torch.uint8, device=dev)
+    out = torch.empty((T, d), dtype=sets[0]["x"].dtype, device=dev)
+    scale = 1.0 / C
+    stream = torch.cuda.current_stream()
+
+    def ptr(t):
+        return None if t is None else t.data_ptr()
+
+    calls = [(dtc, C, T, d, E, k, F, ptr(st["x"]), ptr(st["w_router"]), ptr(st["bias"]),
+              ptr(st["w_gate"]), ptr(st["w_up"]), ptr(st["w_down"]), scale, ptr(out), ptr(ws),
+              ws_n) for st in sets]
+
+    def step(i, s):
+        rc = L.foe_cluster_block(*calls[i % nsets], s)
+        if rc != 0:
+            raise RuntimeError(foe.last_error())
+
+    # experts that received rows (for the weight-streaming bytes); outside timing
+    e_touched = []
+    for h in range(C):
+        st = sets[0]
+        idx, _ = foe.route(st["x"], st["w_router"][h], None if st["bias"] is None else st["bias"][h], k)
+        p = foe.permute(idx, st["x"], E)
+        e_touched.append(int((p["counts"] > 0).sum().item()))
+    e_touched = sum(e_touched) / C
+
+    def timed(n_steps, run):
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for i in range(n_steps):
+            run(i)
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b)
+
+    sraw = stream.cuda_stream
+    for i in range(args.warmup):
+        step(i, sraw)
+    eager_ms = timed(args.steps, lambda i: step(i, sraw)) / args.steps
+
+    graph_ms = None
+    if not args.no_graph:
+        graphs = []
+        side = torch.cuda.Stream()
+        for i in range(nsets):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                step(i, side.cuda_stream)
+            graphs.append(g)
+        # a replay must reproduce the eager result bit for bit
+        step(0, sraw)
+        torch.cuda.synchronize()
+        ref = out.clone()
+        out.zero_()
+        graphs[0].replay()
+        torch.cuda.synchronize()
+        if not torch.equal(out, ref):
+            raise RuntimeError("graph replay differs from the eager block")
+        for i in range(args.warmup):
+            graphs[i % nsets].replay()
+        graph_ms = timed(args.steps, lambda i: graphs[i % nsets].replay()) / args.steps
+    ms = graph_ms if graph_ms is not None else eager_ms
+
+    # pass B: per-kernel HIP events (eager launches on the same stream)
+    foe.profile_reset()
+    foe.profile_enable(True)
+    t_b = timed(args.steps, lambda i: step(i, sraw))
+    foe.profile_enable(False)
+    kernels = {}
+    for name in foe.profile_names():
+        n, tot = foe.profile_kernel(name)
+        kernels[name] = {"launches": n, "avg_us": round(tot / n * 1e3, 3), "total_ms": tot}
+    foe.profile_reset()
+    dom = max(kernels, key=lambda n: kernels[n]["total_ms"])
+    roof = roofline(dom, cfg, e_touched, kernels[dom]["avg_us"] * 1e-6)
+    per_kernel_roof = {n: roofline(n, cfg, e_touched, v["avg_us"] * 1e-6)
+                       for n, v in kernels.items() if kernel_work(n, cfg, e_touched)[1] > 0}
+
+    ffn_ms = sum(v["total_ms"] for n, v in kernels.items() if n.startswith("ffn")) / args.steps
+    tokens_s = T / (ms * 1e-3)
+    flops = C * (2.0 * T * d * E + 6.0 * T * k * d * F)
+    line = {
+        "metric": METRIC,
+        "value": round(tokens_s, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dt,
+        "data": "synthetic (seeded N(0,1) activations, N(0,sigma) weights; "
+                f"{nsets} rotated input/weight sets)",
+        "config": {"workload": f"{args.config}: C={C} T={T} d={d} E={E} k={k} F={F} {dt}",
+                   "C": C, "T": T, "d": d, "E": E, "k": k, "F": F,
+                   "launch": "hip_graph_replay" if graph_ms is not None else "eager"},
+        "block_tflops": round(flops / (ms * 1e-3) / 1e12, 3),
+        "expert_ffn_tflops": round(6.0 * C * T * k * d * F / (ffn_ms * 1e-3) / 1e12, 3),
+        "eager_ms_per_step": round(eager_ms, 6),
+        "graph_ms_per_step": None if graph_ms is None else round(graph_ms, 6),
+        "profiled_ms_per_step": round(t_b / args.steps, 6),
+        "roofline": roof,
+        "kernels": {n: {"avg_us": v["avg_us"], "launches_per_step": v["launches"] / args.steps,
+                        **({"frac": per_kernel_roof[n]["frac"], "bound": per_kernel_roof[n]["bound"]}
+                           if n in per_kernel_roof else {})}
+                    for n, v in kernels.items()},
+        "cpu_baseline": None,
+    }
+    if args.cpu_seconds > 0:
+        line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

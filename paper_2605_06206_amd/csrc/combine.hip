@@ -1,0 +1,137 @@
+// Weighted un-permute-combine (Table 3 "MoE update") and the local reduction
+// of cluster partials (Table 3 "Cross-group avg."; Section 3.2).  Both are
+// HBM-bound row streams: one wave per token row, 128-bit loads and stores,
+// fp32 accumulation in a fixed order.
+#include "foe_common.hpp"
+
+namespace foe {
+namespace {
+
+template <typename T>
+__global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
+                                                      const int32_t* __restrict__ row_of,
+                                                      const float* __restrict__ w,
+                                                      const T* __restrict__ res, int T_, int d,
+                                                      int k, T* __restrict__ out) {
+  constexpr int EPV = Vec16<T>::N;
+  constexpr int U = 2;  // row chunks per lane in flight
+  const int lane = lane_id();
+  const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (tok >= T_) return;
+  const int R = T_ * k;
+  const int nvec = d / EPV;
+  for (int c0 = 0; c0 < nvec; c0 += U * kWave) {
+    float acc[U][EPV];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int v = 0; v < EPV; ++v) acc[u][v] = 0.f;
+    for (int j = 0; j < k; ++j) {
+      const int p = row_of[(size_t)tok * k + j];
+      const float wj = w[(size_t)tok * k + j];
+      if (p < 0 || p >= R) continue;
+      const T* src = y + (size_t)p * d;
+      Vec16<T> v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c = c0 + u * kWave + lane;
+        if (c < nvec) v[u] = load16_cached(src + (size_t)c * EPV);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) acc[u][e] = fmaf(wj, to_f32(v[u].v[e]), acc[u][e]);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + u * kWave + lane;
+      if (c >= nvec) continue;
+      Vec16<T> o;
+      if (res != nullptr) {
+        Vec16<T> r = load16_cached(res + (size_t)tok * d + (size_t)c * EPV);
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) o.v[e] = from_f32<T>(to_f32(r.v[e]) + acc[u][e]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) o.v[e] = from_f32<T>(acc[u][e]);
+      }
+      store16(out + (size_t)tok * d + (size_t)c * EPV, o);
+    }
+  }
+}
+
+// out = scale * sum_h (res + P_h), h = 0..C-1 in order; one 16-byte vector per
+// thread per grid-stride step.
+template <typename T>
+__global__ __launch_bounds__(256) void reduce_kernel(const T* __restrict__ P,
+                                                     const T* __restrict__ res, float scale,
+                                                     int C, long long nvec, long long plane,
+                                                     T* __restrict__ out) {
+  constexpr int EPV = Vec16<T>::N;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < nvec;
+       i += (long long)gridDim.x * blockDim.x) {
+    float acc[EPV];
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) acc[e] = 0.f;
+    float r[EPV];
+    if (res != nullptr) {
+      Vec16<T> rv = load16_cached(res + i * EPV);
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) r[e] = to_f32(rv.v[e]);
+    }
+    for (int h = 0; h < C; ++h) {
+      Vec16<T> pv = load16_cached(P + (size_t)h * plane + i * EPV);
+#pragma unroll
+      for (int e = 0; e < EPV; ++e)
+        acc[e] += (res != nullptr) ? (r[e] + to_f32(pv.v[e])) : to_f32(pv.v[e]);
+    }
+    Vec16<T> o;
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) o.v[e] = from_f32<T>(scale * acc[e]);
+    store16(out + i * EPV, o);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_combine(foe_dtype dt, int T, int d, int k, const void* y_perm,
+                          const int32_t* row_of, const float* topk_w, const void* residual,
+                          void* out, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  dim3 grid(ceil_div(T, 4));
+  ProfileScope ps("combine", s);
+  if (dt == FOE_BF16)
+    hipLaunchKernelGGL(combine_kernel<bf16>, grid, dim3(256), 0, s,
+                       reinterpret_cast<const bf16*>(y_perm), row_of, topk_w,
+                       reinterpret_cast<const bf16*>(residual), T, d, k,
+                       reinterpret_cast<bf16*>(out));
+  else
+    hipLaunchKernelGGL(combine_kernel<float>, grid, dim3(256), 0, s,
+                       reinterpret_cast<const float*>(y_perm), row_of, topk_w,
+                       reinterpret_cast<const float*>(residual), T, d, k,
+                       reinterpret_cast<float*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce(foe_dtype dt, int C, int T, int d, const void* partials,
+                         const void* residual, float scale, void* out, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const long long plane = (long long)T * d;
+  const long long nvec = plane / (dt == FOE_BF16 ? 8 : 4);
+  const long long want = (nvec + 255) / 256;
+  dim3 grid((unsigned)(want < 8192 ? want : 8192));
+  ProfileScope ps("reduce", s);
+  if (dt == FOE_BF16)
+    hipLaunchKernelGGL(reduce_kernel<bf16>, grid, dim3(256), 0, s,
+                       reinterpret_cast<const bf16*>(partials),
+                       reinterpret_cast<const bf16*>(residual), scale, C, nvec, plane,
+                       reinterpret_cast<bf16*>(out));
+  else
+    hipLaunchKernelGGL(reduce_kernel<float>, grid, dim3(256), 0, s,
+                       reinterpret_cast<const float*>(partials),
+                       reinterpret_cast<const float*>(residual), scale, C, nvec, plane,
+                       reinterpret_cast<float*>(out));
+  return hipGetLastError();
+}
+
+}  // namespace foe

@@ -1,0 +1,420 @@
+// C ABI of the per-cluster MoE block library (declarations and contracts in
+// include/foe.h).  Host code only: argument checks, workspace carving, the
+// per-cluster launch sequence and the kernel-timing registry.
+#include <limits.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "foe_common.hpp"
+
+namespace foe {
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+  return fail(FOE_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+size_t esize(foe_dtype dt) { return dt == FOE_BF16 ? 2 : 4; }
+
+// ---- argument checks --------------------------------------------------------
+struct Check {
+  std::string err;
+  void need(bool ok, const char* msg) {
+    if (!ok && err.empty()) err = msg;
+  }
+  void tensor(const void* p, bool required, const char* name) {
+    if (!err.empty()) return;
+    if (p == nullptr) {
+      if (required) err = std::string(name) + " is NULL";
+    } else if (!aligned16(p)) {
+      err = std::string(name) + " is not 16-byte aligned";
+    }
+  }
+  void small(const void* p, bool required, const char* name) {
+    if (!err.empty()) return;
+    if (p == nullptr) {
+      if (required) err = std::string(name) + " is NULL";
+    } else if (!aligned4(p)) {
+      err = std::string(name) + " is not 4-byte aligned";
+    }
+  }
+};
+
+void check_dtype(Check& c, foe_dtype dt) {
+  c.need(dt == FOE_F32 || dt == FOE_BF16, "dt must be FOE_F32 or FOE_BF16");
+}
+void check_dim8(Check& c, int v, const char* msg) { c.need(v >= 8 && v % 8 == 0, msg); }
+void check_route_shape(Check& c, int T, int E, int k) {
+  c.need(T >= 0, "T must be >= 0");
+  c.need(E >= 1 && E <= 256, "E must be in [1, 256]");
+  c.need(k >= 1 && k <= E, "k must be in [1, E]");
+  c.need((long long)T * (k < 1 ? 1 : k) <= INT_MAX, "T*k must fit in int32");
+}
+
+// ---- workspace layout of foe_cluster_block ---------------------------------
+struct BlockWs {
+  size_t topk_idx, topk_w, counts, offsets, sorted_src, row_of, x_perm, y, perm, ffn, deltas, total;
+};
+
+BlockWs block_ws(foe_dtype dt, int C, int T, int d, int E, int k, int F) {
+  BlockWs w{};
+  const size_t R = (size_t)T * k, s = esize(dt);
+  size_t off = 0;
+  auto take = [&](size_t& field, size_t bytes) {
+    off = align_up(off, 256);
+    field = off;
+    off += bytes;
+  };
+  take(w.topk_idx, R * 4);
+  take(w.topk_w, R * 4);
+  take(w.counts, (size_t)E * 4);
+  take(w.offsets, (size_t)(E + 1) * 4);
+  take(w.sorted_src, R * 4);
+  take(w.row_of, R * 4);
+  take(w.x_perm, R * d * s);
+  take(w.y, R * d * s);
+  take(w.perm, permute_scratch_bytes(T, k, E));
+  take(w.ffn, ffn_scratch_bytes(dt, (int)R, F));
+  take(w.deltas, (size_t)C * T * d * s);
+  w.total = align_up(off, 256);
+  return w;
+}
+
+// ---- kernel timing registry -------------------------------------------------
+struct ProfRec {
+  std::string name;
+  int ev;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<hipEvent_t> g_events;  // pairs (2*ev, 2*ev+1), reused across resets
+size_t g_events_used = 0;
+std::vector<ProfRec> g_recs;
+
+}  // namespace
+
+int profile_begin(const char* name, hipStream_t stream) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  if (!g_prof_on) return -1;
+  if (g_events_used * 2 + 2 > g_events.size()) {
+    hipEvent_t a, b;
+    if (hipEventCreate(&a) != hipSuccess) return -1;
+    if (hipEventCreate(&b) != hipSuccess) {
+      (void)hipEventDestroy(a);
+      return -1;
+    }
+    g_events.push_back(a);
+    g_events.push_back(b);
+  }
+  const int ev = (int)g_events_used++;
+  g_recs.push_back({name, ev});
+  (void)hipEventRecord(g_events[2 * ev], stream);
+  return ev;
+}
+
+void profile_end(int slot, hipStream_t stream) {
+  if (slot < 0) return;
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  (void)hipEventRecord(g_events[2 * slot + 1], stream);
+}
+
+}  // namespace foe
+
+using namespace foe;
+
+extern "C" {
+
+const char* foe_last_error(void) { return g_err.c_str(); }
+
+size_t foe_workspace_bytes(const char* op, foe_dtype dt, int C, int T, int d, int E, int k,
+                           int F) {
+  if (op == nullptr) {
+    g_err = "op is NULL";
+    return SIZE_MAX;
+  }
+  const std::string o(op);
+  Check c;
+  check_dtype(c, dt);
+  if (o == "route" || o == "combine" || o == "reduce") {
+    if (!c.err.empty()) return (g_err = c.err, SIZE_MAX);
+    return 0;
+  }
+  if (o == "permute") {
+    check_route_shape(c, T, E, k);
+    if (!c.err.empty()) return (g_err = c.err, SIZE_MAX);
+    return permute_scratch_bytes(T, k, E);
+  }
+  if (o == "expert_ffn") {
+    c.need(T >= 0 && k >= 1 && (long long)T * k <= INT_MAX, "rows = T*k must be in [0, 2^31)");
+    check_dim8(c, F, "F must be a positive multiple of 8");
+    if (!c.err.empty()) return (g_err = c.err, SIZE_MAX);
+    return ffn_scratch_bytes(dt, T * k, F);
+  }
+  if (o == "cluster_block") {
+    check_route_shape(c, T, E, k);
+    c.need(C >= 1 && C <= 64, "C must be in [1, 64]");
+    check_dim8(c, d, "d must be a positive multiple of 8");
+    check_dim8(c, F, "F must be a positive multiple of 8");
+    if (!c.err.empty()) return (g_err = c.err, SIZE_MAX);
+    return block_ws(dt, C, T, d, E, k, F).total;
+  }
+  g_err = "unknown op '" + o + "'";
+  return SIZE_MAX;
+}
+
+int foe_route(foe_dtype dt, int T, int d, int E, int k, const void* x, const void* w_router,
+              const float* bias, int32_t* topk_idx, float* topk_w, void* stream) {
+  Check c;
+  check_dtype(c, dt);
+  check_route_shape(c, T, E, k);
+  check_dim8(c, d, "d must be a positive multiple of 8");
+  const bool any = T > 0;
+  c.tensor(x, any, "x");
+  c.tensor(w_router, any, "w_router");
+  c.small(bias, false, "bias");
+  c.small(topk_idx, any, "topk_idx");
+  c.small(topk_w, any, "topk_w");
+  if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_route: " + c.err);
+  hipError_t e = launch_route(dt, T, d, E, k, x, w_router, bias, topk_idx, topk_w,
+                              reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "foe_route");
+  return FOE_OK;
+}
+
+int foe_permute(foe_dtype dt, int T, int d, int E, int k, const int32_t* topk_idx, const void* x,
+                int32_t* expert_counts, int32_t* expert_offsets, int32_t* sorted_src,
+                int32_t* row_of, void* x_perm, void* ws, size_t ws_bytes, void* stream) {
+  Check c;
+  check_dtype(c, dt);
+  check_route_shape(c, T, E, k);
+  check_dim8(c, d, "d must be a positive multiple of 8");
+  const bool any = T > 0;
+  c.small(topk_idx, any, "topk_idx");
+  c.tensor(x, any, "x");
+  c.small(expert_counts, false, "expert_counts");
+  c.small(expert_offsets, true, "expert_offsets");
+  c.small(sorted_src, any, "sorted_src");
+  c.small(row_of, any, "row_of");
+  c.tensor(x_perm, any, "x_perm");
+  if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_permute: " + c.err);
+  const size_t need = permute_scratch_bytes(T, k, E);
+  if (need > 0 && (ws == nullptr || !aligned16(ws)))
+    return fail(FOE_ERR_INVALID, "foe_permute: ws is NULL or not 16-byte aligned");
+  if (ws_bytes < need)
+    return fail(FOE_ERR_WORKSPACE, "foe_permute: workspace needs " + std::to_string(need) +
+                                       " bytes, got " + std::to_string(ws_bytes));
+  hipError_t e = launch_permute(dt, T, d, E, k, topk_idx, x, expert_counts, expert_offsets,
+                                sorted_src, row_of, x_perm, ws,
+                                reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "foe_permute");
+  return FOE_OK;
+}
+
+int foe_expert_ffn(foe_dtype dt, int E, int d, int F, int rows, const void* x_perm,
+                   const int32_t* expert_offsets, const void* w_gate, const void* w_up,
+                   const void* w_down, void* y_perm, void* ws, size_t ws_bytes, void* stream) {
+  Check c;
+  check_dtype(c, dt);
+  c.need(E >= 1 && E <= 256, "E must be in [1, 256]");
+  c.need(rows >= 0, "rows must be >= 0");
+  check_dim8(c, d, "d must be a positive multiple of 8");
+  check_dim8(c, F, "F must be a positive multiple of 8");
+  const bool any = rows > 0;
+  c.tensor(x_perm, any, "x_perm");
+  c.small(expert_offsets, any, "expert_offsets");
+  c.tensor(w_gate, any, "w_gate");
+  c.tensor(w_up, any, "w_up");
+  c.tensor(w_down, any, "w_down");
+  c.tensor(y_perm, any, "y_perm");
+  if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_expert_ffn: " + c.err);
+  const size_t need = any ? ffn_scratch_bytes(dt, rows, F) : 0;
+  if (need > 0 && (ws == nullptr || !aligned16(ws)))
+    return fail(FOE_ERR_INVALID, "foe_expert_ffn: ws is NULL or not 16-byte aligned");
+  if (ws_bytes < need)
+    return fail(FOE_ERR_WORKSPACE, "foe_expert_ffn: workspace needs " + std::to_string(need) +
+                                       " bytes, got " + std::to_string(ws_bytes));
+  hipError_t e = launch_expert_ffn(dt, E, d, F, rows, x_perm, expert_offsets, w_gate, w_up,
+                                   w_down, y_perm, ws, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "foe_expert_ffn");
+  return FOE_OK;
+}
+
+int foe_combine(foe_dtype dt, int T, int d, int k, const void* y_perm, const int32_t* row_of,
+                const float* topk_w, const void* residual, void* out, void* stream) {
+  Check c;
+  check_dtype(c, dt);
+  c.need(T >= 0, "T must be >= 0");
+  c.need(k >= 1 && k <= 256, "k must be in [1, 256]");
+  c.need((long long)T * (k < 1 ? 1 : k) <= INT_MAX, "T*k must fit in int32");
+  check_dim8(c, d, "d must be a positive multiple of 8");
+  const bool any = T > 0;
+  c.tensor(y_perm, any, "y_perm");
+  c.small(row_of, any, "row_of");
+  c.small(topk_w, any, "topk_w");
+  c.tensor(residual, false, "residual");
+  c.tensor(out, any, "out");
+  if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_combine: " + c.err);
+  hipError_t e = launch_combine(dt, T, d, k, y_perm, row_of, topk_w, residual, out,
+                                reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "foe_combine");
+  return FOE_OK;
+}
+
+int foe_reduce(foe_dtype dt, int C, int T, int d, const void* partials, const void* residual,
+               float scale, void* out, void* stream) {
+  Check c;
+  check_dtype(c, dt);
+  c.need(C >= 1 && C <= 64, "C must be in [1, 64]");
+  c.need(T >= 0, "T must be >= 0");
+  check_dim8(c, d, "d must be a positive multiple of 8");
+  const bool any = T > 0;
+  c.tensor(partials, any, "partials");
+  c.tensor(residual, false, "residual");
+  c.tensor(out, any, "out");
+  if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_reduce: " + c.err);
+  hipError_t e = launch_reduce(dt, C, T, d, partials, residual, scale, out,
+                               reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "foe_reduce");
+  return FOE_OK;
+}
+
+int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F, const void* x,
+                      const void* w_router, const float* bias, const void* w_gate,
+                      const void* w_up, const void* w_down, float reduce_scale, void* out,
+                      void* ws, size_t ws_bytes, void* stream) {
+  Check c;
+  check_dtype(c, dt);
+  c.need(C >= 1 && C <= 64, "C must be in [1, 64]");
+  check_route_shape(c, T, E, k);
+  check_dim8(c, d, "d must be a positive multiple of 8");
+  check_dim8(c, F, "F must be a positive multiple of 8");
+  const bool any = T > 0;
+  c.tensor(x, any, "x");
+  c.tensor(w_router, any, "w_router");
+  c.small(bias, false, "bias");
+  c.tensor(w_gate, any, "w_gate");
+  c.tensor(w_up, any, "w_up");
+  c.tensor(w_down, any, "w_down");
+  c.tensor(out, any, "out");
+  if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_cluster_block: " + c.err);
+  if (!any) return FOE_OK;
+  const BlockWs L = block_ws(dt, C, T, d, E, k, F);
+  if (ws == nullptr || !aligned16(ws))
+    return fail(FOE_ERR_INVALID, "foe_cluster_block: ws is NULL or not 16-byte aligned");
+  if (ws_bytes < L.total)
+    return fail(FOE_ERR_WORKSPACE, "foe_cluster_block: workspace needs " +
+                                       std::to_string(L.total) + " bytes, got " +
+                                       std::to_string(ws_bytes));
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  unsigned char* base = reinterpret_cast<unsigned char*>(ws);
+  int32_t* topk_idx = reinterpret_cast<int32_t*>(base + L.topk_idx);
+  float* topk_w = reinterpret_cast<float*>(base + L.topk_w);
+  int32_t* counts = reinterpret_cast<int32_t*>(base + L.counts);
+  int32_t* offsets = reinterpret_cast<int32_t*>(base + L.offsets);
+  int32_t* sorted_src = reinterpret_cast<int32_t*>(base + L.sorted_src);
+  int32_t* row_of = reinterpret_cast<int32_t*>(base + L.row_of);
+  void* x_perm = base + L.x_perm;
+  void* y = base + L.y;
+  void* perm_ws = base + L.perm;
+  void* ffn_ws = base + L.ffn;
+  unsigned char* deltas = base + L.deltas;
+
+  const size_t s_el = esize(dt);
+  const int R = T * k;
+  const bool direct = (C == 1 && reduce_scale == 1.0f);  // out = x + delta in one pass
+  const unsigned char* wr = reinterpret_cast<const unsigned char*>(w_router);
+  const unsigned char* wg = reinterpret_cast<const unsigned char*>(w_gate);
+  const unsigned char* wu = reinterpret_cast<const unsigned char*>(w_up);
+  const unsigned char* wd = reinterpret_cast<const unsigned char*>(w_down);
+  for (int h = 0; h < C; ++h) {
+    const size_t wr_off = (size_t)h * E * d * s_el;
+    const size_t wx_off = (size_t)h * E * F * d * s_el;
+    hipError_t e = launch_route(dt, T, d, E, k, x, wr + wr_off,
+                                bias ? bias + (size_t)h * E : nullptr, topk_idx, topk_w, s);
+    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/route");
+    e = launch_permute(dt, T, d, E, k, topk_idx, x, counts, offsets, sorted_src, row_of, x_perm,
+                       perm_ws, s);
+    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/permute");
+    e = launch_expert_ffn(dt, E, d, F, R, x_perm, offsets, wg + wx_off, wu + wx_off,
+                          wd + wx_off, y, ffn_ws, s);
+    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/expert_ffn");
+    if (direct)
+      e = launch_combine(dt, T, d, k, y, row_of, topk_w, x, out, s);
+    else
+      e = launch_combine(dt, T, d, k, y, row_of, topk_w, nullptr,
+                         deltas + (size_t)h * T * d * s_el, s);
+    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/combine");
+  }
+  if (!direct) {
+    hipError_t e = launch_reduce(dt, C, T, d, deltas, x, reduce_scale, out, s);
+    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/reduce");
+  }
+  return FOE_OK;
+}
+
+int foe_profile_enable(int on) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  g_prof_on = on != 0;
+  return FOE_OK;
+}
+
+int foe_profile_reset(void) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  g_recs.clear();
+  g_events_used = 0;
+  return FOE_OK;
+}
+
+int foe_profile_kernel(const char* name, int* launches, double* total_ms) {
+  if (name == nullptr || launches == nullptr || total_ms == nullptr)
+    return fail(FOE_ERR_INVALID, "foe_profile_kernel: NULL argument");
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  int n = 0;
+  double ms = 0.0;
+  for (const ProfRec& r : g_recs) {
+    if (r.name != name) continue;
+    hipEvent_t a = g_events[2 * r.ev], b = g_events[2 * r.ev + 1];
+    hipError_t e = hipEventSynchronize(b);
+    if (e != hipSuccess) return hip_fail(e, "foe_profile_kernel");
+    float t = 0.f;
+    e = hipEventElapsedTime(&t, a, b);
+    if (e != hipSuccess) return hip_fail(e, "foe_profile_kernel");
+    ms += t;
+    ++n;
+  }
+  if (n == 0) return fail(FOE_ERR_INVALID, std::string("no recorded launch of ") + name);
+  *launches = n;
+  *total_ms = ms;
+  return FOE_OK;
+}
+
+int foe_profile_names(char* buf, size_t len) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  std::string all;
+  for (const ProfRec& r : g_recs) {
+    const std::string key = "," + r.name + ",";
+    if (("," + all + ",").find(key) != std::string::npos) continue;
+    if (!all.empty()) all += ",";
+    all += r.name;
+  }
+  if (buf != nullptr && len > 0) {
+    const size_t n = all.size() < len - 1 ? all.size() : len - 1;
+    all.copy(buf, n);
+    buf[n] = '\0';
+  }
+  return (int)all.size() + 1;
+}
+
+}  // extern "C"

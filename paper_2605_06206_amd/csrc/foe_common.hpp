@@ -1,0 +1,102 @@
+// Shared device/host helpers of the gfx950 per-cluster MoE block library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "foe.h"
+
+namespace foe {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+// ---- element conversion --------------------------------------------------
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+// hardware v_cvt_pk_bf16_f32: round to nearest even
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }
+
+// A 16-byte vector of elements of type T (8 bf16 or 4 fp32).
+template <typename T> struct Vec16 {
+  static constexpr int N = 16 / sizeof(T);
+  T v[N];
+};
+
+template <typename T>
+__device__ __forceinline__ Vec16<T> load16(const T* p) {
+  Vec16<T> r;
+  *reinterpret_cast<u32x4*>(r.v) = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return r;
+}
+template <typename T>
+__device__ __forceinline__ Vec16<T> load16_cached(const T* p) {
+  Vec16<T> r;
+  *reinterpret_cast<u32x4*>(r.v) = *reinterpret_cast<const u32x4*>(p);
+  return r;
+}
+template <typename T>
+__device__ __forceinline__ void store16(T* p, const Vec16<T>& r) {
+  *reinterpret_cast<u32x4*>(p) = *reinterpret_cast<const u32x4*>(r.v);
+}
+__device__ __forceinline__ u32x4 zero_u32x4() { return u32x4{0u, 0u, 0u, 0u}; }
+
+// ---- wave helpers ----------------------------------------------------------
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+// Rotate a 32-bit value right by `sh` lanes inside each row of 16 lanes (DPP).
+template <int SH>
+__device__ __forceinline__ int row_ror(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, 0x120 + SH, 0xF, 0xF, false);
+}
+
+// ---- host side: launch bookkeeping ----------------------------------------
+// Kernel timing hooks (see foe_profile_* in foe.h).  `begin` returns an opaque
+// slot index or -1 when timing is off; `end` closes it.
+int profile_begin(const char* name, hipStream_t stream);
+void profile_end(int slot, hipStream_t stream);
+
+struct ProfileScope {
+  int slot;
+  hipStream_t stream;
+  ProfileScope(const char* name, hipStream_t s) : slot(profile_begin(name, s)), stream(s) {}
+  ~ProfileScope() { profile_end(slot, stream); }
+};
+
+inline int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// ---- kernel launchers (one translation unit each) -------------------------
+hipError_t launch_route(foe_dtype dt, int T, int d, int E, int k, const void* x,
+                        const void* w_router, const float* bias, int32_t* topk_idx,
+                        float* topk_w, hipStream_t s);
+
+// permute scratch = 2 * nblk * E int32 (see permute_blocks())
+int permute_blocks(int R);
+size_t permute_scratch_bytes(int T, int k, int E);
+hipError_t launch_permute(foe_dtype dt, int T, int d, int E, int k, const int32_t* topk_idx,
+                          const void* x, int32_t* counts, int32_t* offsets, int32_t* sorted_src,
+                          int32_t* row_of, void* x_perm, void* scratch, hipStream_t s);
+
+size_t ffn_scratch_bytes(foe_dtype dt, int rows, int F);
+hipError_t launch_expert_ffn(foe_dtype dt, int E, int d, int F, int rows, const void* x_perm,
+                             const int32_t* offsets, const void* w_gate, const void* w_up,
+                             const void* w_down, void* y_perm, void* scratch, hipStream_t s);
+
+hipError_t launch_combine(foe_dtype dt, int T, int d, int k, const void* y_perm,
+                          const int32_t* row_of, const float* topk_w, const void* residual,
+                          void* out, hipStream_t s);
+hipError_t launch_reduce(foe_dtype dt, int C, int T, int d, const void* partials,
+                         const void* residual, float scale, void* out, hipStream_t s);
+hipError_t launch_fill_i32(int32_t* p, int n, int32_t v, hipStream_t s);
+
+}  // namespace foe

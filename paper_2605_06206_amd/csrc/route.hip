@@ -1,0 +1,209 @@
+// Router scores + per-group top-k + softmax weights (Section 3.1, routing
+// equation), fused in one kernel: the [T,E] scores never leave the chip.
+//
+// One workgroup = 4 waves = 16 tokens.  The score tile S[16 tokens][E] is a
+// skinny GEMM x[16,d] * W_r[E,d]^T on MFMA (bf16: 16x16x32, fp32: 16x16x4)
+// with K split across the 4 waves; the 4 partial tiles are summed in LDS in a
+// fixed order.  In the 16x16 MFMA result layout each row of 16 lanes holds all
+// 16 experts of one token (per accumulator register), so the top-k is k rounds
+// of a (score desc, id asc) arg-max across a 16-lane row with DPP rotations.
+#include "foe_common.hpp"
+
+namespace foe {
+namespace {
+
+constexpr int kTok = 16;    // tokens per workgroup
+constexpr int kWaves = 4;   // K split
+
+// (v, e) beats (w, f): larger score, equal scores -> lower id
+__device__ __forceinline__ bool beats(float v, int e, float w, int f) {
+  return v > w || (v == w && e < f);
+}
+
+template <int SH>
+__device__ __forceinline__ void argmax_step(float& bv, int& be) {
+  float ov = __int_as_float(row_ror<SH>(__float_as_int(bv)));
+  int oe = row_ror<SH>(be);
+  if (beats(ov, oe, bv, be)) { bv = ov; be = oe; }
+}
+
+template <typename T> struct RouteMma;
+
+// bf16: each MFMA step consumes 32 k; lane (r = l%16, q = l/16) supplies
+// x[r][kc + 8q .. +8) and W_r[e][same k] — the same k map on both operands.
+template <> struct RouteMma<bf16> {
+  static constexpr int KSTEP = 32;
+  template <int NT>
+  __device__ static void run(const bf16* x, const bf16* w, int T, int d, int E, int t0,
+                             int wave, int lane, f32x4 (&acc)[NT]) {
+    const int r = lane & 15, q = lane >> 4;
+    const int tok = t0 + r;
+    const bool tok_ok = tok < T;
+    const bf16* xrow = x + (size_t)(tok_ok ? tok : 0) * d;
+    const int nsteps = (d + KSTEP - 1) / KSTEP;
+    for (int c = wave; c < nsteps; c += kWaves) {
+      const int kb = c * KSTEP + q * 8;
+      const bool k_ok = kb < d;
+      u32x4 a = (tok_ok && k_ok) ? *reinterpret_cast<const u32x4*>(xrow + kb) : zero_u32x4();
+      u32x4 b[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int e = nt * 16 + r;
+        b[nt] = (e < E && k_ok) ? *reinterpret_cast<const u32x4*>(w + (size_t)e * d + kb)
+                                : zero_u32x4();
+      }
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b[nt]), acc[nt], 0, 0, 0);
+    }
+  }
+};
+
+// fp32: 16x16x4 MFMA; a lane loads 4 consecutive k and issues 4 MFMAs, the
+// s-th using element s (k map kc + 4q + s on both operands).
+template <> struct RouteMma<float> {
+  static constexpr int KSTEP = 16;
+  template <int NT>
+  __device__ static void run(const float* x, const float* w, int T, int d, int E, int t0,
+                             int wave, int lane, f32x4 (&acc)[NT]) {
+    const int r = lane & 15, q = lane >> 4;
+    const int tok = t0 + r;
+    const bool tok_ok = tok < T;
+    const float* xrow = x + (size_t)(tok_ok ? tok : 0) * d;
+    const int nsteps = (d + KSTEP - 1) / KSTEP;
+    for (int c = wave; c < nsteps; c += kWaves) {
+      const int kb = c * KSTEP + q * 4;
+      const bool k_ok = kb < d;
+      f32x4 a = (tok_ok && k_ok) ? *reinterpret_cast<const f32x4*>(xrow + kb)
+                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int e = nt * 16 + r;
+        f32x4 b = (e < E && k_ok) ? *reinterpret_cast<const f32x4*>(w + (size_t)e * d + kb)
+                                  : f32x4{0.f, 0.f, 0.f, 0.f};
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], acc[nt], 0, 0, 0);
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], acc[nt], 0, 0, 0);
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], acc[nt], 0, 0, 0);
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], acc[nt], 0, 0, 0);
+      }
+    }
+  }
+};
+
+template <typename T, int NT>
+__global__ __launch_bounds__(256) void route_kernel(const T* __restrict__ x,
+                                                    const T* __restrict__ w,
+                                                    const float* __restrict__ bias, int T_,
+                                                    int d, int E, int k,
+                                                    int32_t* __restrict__ topk_idx,
+                                                    float* __restrict__ topk_w) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int t0 = blockIdx.x * kTok;
+
+  f32x4 acc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  RouteMma<T>::template run<NT>(x, w, T_, d, E, t0, wave, lane, acc);
+
+  // partial tiles of the 4 waves -> LDS [wave][nt][lane] (f32x4)
+  f32x4* part = reinterpret_cast<f32x4*>(smem);
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) part[(wave * NT + nt) * kWave + lane] = acc[nt];
+  __syncthreads();
+
+  // wave `wave` owns accumulator register i = wave: token 4*(lane/16) + wave,
+  // expert nt*16 + lane%16.  Sum the 4 partials in wave order.
+  const int col = lane & 15;
+  const int tl = 4 * (lane >> 4) + wave;  // token within the workgroup
+  float g[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float s = 0.f;
+#pragma unroll
+    for (int w4 = 0; w4 < kWaves; ++w4) s += part[(w4 * NT + nt) * kWave + lane][wave];
+    const int e = nt * 16 + col;
+    if (bias != nullptr && e < E) s += bias[e];
+    g[nt] = s;
+  }
+  __syncthreads();  // partial tiles are dead; LDS is reused for the selection
+
+  int* sel_e = reinterpret_cast<int*>(smem);
+  float* sel_v = reinterpret_cast<float*>(smem) + kTok * k;
+
+  unsigned taken = 0;  // bit nt: expert nt*16 + col already selected / absent
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+    if (nt * 16 + col >= E) taken |= 1u << nt;
+
+  for (int s = 0; s < k; ++s) {
+    float bv = -__builtin_inff();
+    int be = 0x7fffffff;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int e = nt * 16 + col;
+      if (!((taken >> nt) & 1u) && beats(g[nt], e, bv, be)) { bv = g[nt]; be = e; }
+    }
+    argmax_step<8>(bv, be);
+    argmax_step<4>(bv, be);
+    argmax_step<2>(bv, be);
+    argmax_step<1>(bv, be);
+    if (be != 0x7fffffff && (be & 15) == col) taken |= 1u << (be >> 4);
+    if (col == 0) {
+      sel_e[tl * k + s] = (be == 0x7fffffff) ? -1 : be;
+      sel_v[tl * k + s] = bv;
+    }
+  }
+  __syncthreads();
+
+  // softmax over the selected scores; lane col writes slots col, col+16, ...
+  const int tok = t0 + tl;
+  if (tok < T_) {
+    const float m = sel_v[tl * k];
+    float z = 0.f;
+    for (int s = 0; s < k; ++s) z += expf(sel_v[tl * k + s] - m);
+    const float inv = 1.0f / z;
+    for (int s = col; s < k; s += 16) {
+      topk_idx[(size_t)tok * k + s] = sel_e[tl * k + s];
+      topk_w[(size_t)tok * k + s] = expf(sel_v[tl * k + s] - m) * inv;
+    }
+  }
+}
+
+template <typename T, int NT>
+hipError_t launch_nt(int T_, int d, int E, int k, const void* x, const void* w,
+                     const float* bias, int32_t* idx, float* wt, hipStream_t s) {
+  size_t lds_red = (size_t)kWaves * NT * kWave * sizeof(f32x4);
+  size_t lds_sel = (size_t)kTok * k * 8;
+  size_t lds = lds_red > lds_sel ? lds_red : lds_sel;
+  dim3 grid(ceil_div(T_, kTok));
+  ProfileScope ps("route", s);
+  hipLaunchKernelGGL((route_kernel<T, NT>), grid, dim3(256), lds, s,
+                     reinterpret_cast<const T*>(x), reinterpret_cast<const T*>(w), bias, T_, d,
+                     E, k, idx, wt);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_t(int T_, int d, int E, int k, const void* x, const void* w, const float* bias,
+                    int32_t* idx, float* wt, hipStream_t s) {
+  if (E <= 16) return launch_nt<T, 1>(T_, d, E, k, x, w, bias, idx, wt, s);
+  if (E <= 32) return launch_nt<T, 2>(T_, d, E, k, x, w, bias, idx, wt, s);
+  if (E <= 64) return launch_nt<T, 4>(T_, d, E, k, x, w, bias, idx, wt, s);
+  if (E <= 128) return launch_nt<T, 8>(T_, d, E, k, x, w, bias, idx, wt, s);
+  return launch_nt<T, 16>(T_, d, E, k, x, w, bias, idx, wt, s);
+}
+
+}  // namespace
+
+hipError_t launch_route(foe_dtype dt, int T, int d, int E, int k, const void* x,
+                        const void* w_router, const float* bias, int32_t* topk_idx,
+                        float* topk_w, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (dt == FOE_BF16) return launch_t<bf16>(T, d, E, k, x, w_router, bias, topk_idx, topk_w, s);
+  return launch_t<float>(T, d, E, k, x, w_router, bias, topk_idx, topk_w, s);
+}
+
+}  // namespace foe

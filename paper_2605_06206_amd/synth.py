@@ -91,8 +91,8 @@ def make_cluster_weights(E, d, F, sigma, seed, h, dtype, bias=None):
 def make_block_inputs(cfg, T=None, weight_set=0):
     """Inputs of one block invocation for a config (name or dict).
 
-    ``x ~ N(0,1) [T,d]`` from ``default_rng(seed)``; cluster ``h`` weights from
-    ``default_rng([seed + 7919*weight_set, h])``.  ``T`` may be overridden (the
+    ``x ~ N(0,1) [T,d]`` from ``default_rng(seed + 7919*weight_set)``; cluster
+    ``h`` weights from ``default_rng([seed + 7919*weight_set, h])``.  ``T`` may be overridden (the
     first ``T`` rows of the same draw are not kept: a fresh draw of that size).
     bf16 configs round every tensor to bf16.  Returns a dict with ``cfg``,
     ``x`` (fp32 array) and ``clusters`` (list of weight dicts).
@@ -103,11 +103,11 @@ def make_block_inputs(cfg, T=None, weight_set=0):
         cfg = dict(cfg)
     if T is not None:
         cfg["T"] = T
-    rng = np.random.default_rng(cfg["seed"])
+    wseed = cfg["seed"] + 7919 * weight_set
+    rng = np.random.default_rng(wseed)
     x = rng.standard_normal((cfg["T"], cfg["d"]), dtype=np.float32)
     if cfg["dtype"] == "bf16":
         x = round_to_bf16(x)
-    wseed = cfg["seed"] + 7919 * weight_set
     clusters = [make_cluster_weights(cfg["E"], cfg["d"], cfg["F"], cfg["sigma"],
                                      wseed, h, cfg["dtype"], cfg.get("bias"))
                 for h in range(cfg["C"])]

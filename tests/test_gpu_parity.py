@@ -1,0 +1,450 @@
+"""GPU parity: every entry point of libfoe.so against the CPU oracle on the same
+seeded inputs.
+
+Bars: integer outputs (expert ids, counts, offsets, permutation) bit-exact;
+floating point per tensor max|err| / max|ref| <= 2e-2 (bf16) or 1e-4 (fp32).
+Routing: a token whose fp32 k-th/(k+1)-th score margin (oracle) is below 1e-5
+is exempt from id bit-exactness (both choices are correct); it must still pick
+a valid top-k, and its block output rows are left out of the value comparison.
+Slot order is compared where every adjacent gap among the top k is >= 1e-5.
+"""
+
+import functools
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2605_06206_amd import foe, synth
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+EXEMPT = 1e-5
+DEV = "cuda:0"
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    foe.lib()  # fail loudly if the HIP library is missing
+
+
+def say(*a):
+    print("[gpu-case]", *a, file=sys.stderr, flush=True)
+
+
+def to_dev(a, dtype):
+    a = np.ascontiguousarray(a)
+    if a.dtype in (np.int32, np.int64):
+        return torch.from_numpy(a.astype(np.int32)).to(DEV)
+    if dtype == "bf16":
+        return torch.from_numpy(synth.bf16_bits(a)).to(DEV).view(torch.bfloat16)
+    return torch.from_numpy(a.astype(np.float32)).to(DEV)
+
+
+def host(t):
+    if t.dtype == torch.bfloat16:
+        return t.float().cpu().numpy().astype(np.float64)
+    return t.cpu().numpy()
+
+
+def rel_err(got, ref):
+    ref = np.asarray(ref, np.float64)
+    den = np.max(np.abs(ref))
+    return float(np.max(np.abs(np.asarray(got, np.float64) - ref)) / (den if den > 0 else 1.0))
+
+
+@functools.lru_cache(maxsize=2)
+def cfg_inputs(name):
+    return synth.make_block_inputs(name)
+
+
+def stacked(inp):
+    dt = inp["cfg"]["dtype"]
+    cls = inp["clusters"]
+    w = {key: to_dev(np.stack([c[key] for c in cls]), dt)
+         for key in ("w_router", "w_gate", "w_up", "w_down")}
+    w["bias"] = (to_dev(np.stack([c["bias"] for c in cls]), "f32")
+                 if cls[0]["bias"] is not None else None)
+    return w
+
+
+def check_route(gidx, gw, ref, tol, g64=None):
+    """Compare GPU routing with the oracle's; returns the exempt mask."""
+    gidx = np.asarray(gidx).astype(np.int64)
+    gw = np.asarray(gw, np.float64)
+    exempt = ref["margin"] < EXEMPT
+    ne = ~exempt
+    assert np.array_equal(np.sort(gidx[ne], 1), np.sort(ref["idx"][ne], 1)), "top-k sets differ"
+    ordered = ne & (ref["min_gap"] >= EXEMPT)
+    assert np.array_equal(gidx[ordered], ref["idx"][ordered]), "slot order differs"
+    # weights, aligned by expert id
+    o_g = np.argsort(gidx[ne], 1)
+    o_r = np.argsort(ref["idx"][ne], 1)
+    wg = np.take_along_axis(gw[ne], o_g, 1)
+    wr = np.take_along_axis(ref["w"][ne], o_r, 1)
+    assert rel_err(wg, wr) <= tol, rel_err(wg, wr)
+    # rows of weights sum to one
+    assert np.max(np.abs(gw.sum(1) - 1.0)) <= 1e-5
+    # exempt tokens still pick a valid top-k of the oracle scores
+    g32 = ref["logits"].astype(np.float32).astype(np.float64)
+    k = gidx.shape[1]
+    for t in np.nonzero(exempt)[0]:
+        kth = np.sort(g32[t])[::-1][k - 1]
+        assert len(set(gidx[t])) == k
+        assert np.all(g32[t, gidx[t]] >= kth - EXEMPT)
+    return exempt
+
+
+# ---------------------------------------------------------------------------
+# route
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", synth.CONFIG_ORDER)
+def test_route_parity_configs(name):
+    inp = cfg_inputs(name)
+    cfg = inp["cfg"]
+    dt = cfg["dtype"]
+    x = to_dev(inp["x"], dt)
+    for h, cl in enumerate(inp["clusters"][:2]):
+        say("route", name, "cluster", h, "T", cfg["T"], "d", cfg["d"], "E", cfg["E"], "k", cfg["k"])
+        bias = to_dev(cl["bias"], "f32") if cl["bias"] is not None else None
+        gidx, gw = foe.route(x, to_dev(cl["w_router"], dt), bias, cfg["k"])
+        torch.cuda.synchronize()
+        ref = oracle.route(inp["x"], cl["w_router"], cl["bias"], cfg["k"])
+        exempt = check_route(host(gidx), host(gw), ref, TOL[dt])
+        say("route", name, "cluster", h, "exempt tokens", int(exempt.sum()))
+
+
+@pytest.mark.parametrize("T,d,E,k,dt", [
+    (1, 64, 4, 1, "bf16"), (50, 136, 5, 3, "bf16"), (333, 64, 33, 5, "bf16"),
+    (77, 256, 256, 8, "bf16"), (40, 32, 16, 16, "f32"), (129, 8, 2, 2, "f32"),
+    (300, 512, 64, 64, "bf16"),
+])
+def test_route_parity_shapes(T, d, E, k, dt):
+    """Ragged token tails, K tails (d not a multiple of 32), E not a multiple
+    of 16, E = 256, k = E."""
+    say("route shapes", T, d, E, k, dt)
+    rng = np.random.default_rng(T * 7 + E)
+    xs = rng.standard_normal((T, d)).astype(np.float32)
+    wr = (rng.standard_normal((E, d)) * 0.05).astype(np.float32)
+    bias = (rng.standard_normal(E) * 0.1).astype(np.float32)
+    if dt == "bf16":
+        xs, wr = synth.round_to_bf16(xs), synth.round_to_bf16(wr)
+    gidx, gw = foe.route(to_dev(xs, dt), to_dev(wr, dt), to_dev(bias, "f32"), k)
+    ref = oracle.route(xs, wr, bias, k)
+    check_route(host(gidx), host(gw), ref, TOL[dt])
+
+
+@pytest.mark.parametrize("k", [1, 3])
+def test_route_exact_ties_pick_lower_id(k):
+    """Duplicate router rows give bit-identical scores on both sides: the
+    lower expert id must win, bit-exact, even at the k/(k+1) boundary."""
+    say("route ties k", k)
+    rng = np.random.default_rng(31)
+    T, d, E = 200, 128, 16
+    xs = synth.round_to_bf16(rng.standard_normal((T, d)).astype(np.float32))
+    wr = rng.standard_normal((E, d)).astype(np.float32) * 0.02
+    wr[9] = wr[3] = wr[3] * 8.0  # a strong pair of twins: usually on top
+    wr[12] = wr[5]
+    wr = synth.round_to_bf16(wr)
+    gidx, _ = foe.route(to_dev(xs, "bf16"), to_dev(wr, "bf16"), None, k)
+    gidx = host(gidx)
+    ref = oracle.route(xs, wr, None, k)
+    assert np.array_equal(gidx, ref["idx"])
+    has3 = np.any(gidx == 3, axis=1)
+    has9 = np.any(gidx == 9, axis=1)
+    assert np.all(has3 | ~has9)  # 9 is never chosen without its lower twin 3
+    if k == 1:
+        assert np.sum(gidx[:, 0] == 3) > 0 and not np.any(gidx[:, 0] == 9)
+
+
+# ---------------------------------------------------------------------------
+# permute
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("T,d,E,k,skew,dead,dt", [
+    (37, 64, 7, 3, 1.2, (1,), "bf16"),
+    (3000, 128, 16, 2, 1.2, (), "bf16"),
+    (16384, 4096, 32, 4, 0.0, (), "bf16"),
+    (8192, 2048, 16, 2, 1.2, (), "bf16"),
+    (1025, 32, 256, 8, 0.5, (0, 255), "f32"),
+    (5, 16, 4, 4, 0.0, (), "f32"),
+])
+def test_permute_parity(T, d, E, k, skew, dead, dt):
+    say("permute", T, d, E, k, skew, dead, dt)
+    idx = synth.make_topk_idx(T, E, k, seed=T + E, skew=skew, dead_experts=dead)
+    rng = np.random.default_rng(T)
+    xs = rng.standard_normal((T, d)).astype(np.float32)
+    if dt == "bf16":
+        xs = synth.round_to_bf16(xs)
+    xd = to_dev(xs, dt)
+    got = foe.permute(to_dev(idx, None), xd, E)
+    torch.cuda.synchronize()
+    counts, offsets = oracle.expert_histogram(idx, E)
+    sorted_src, row_of = oracle.permutation(idx)
+    assert np.array_equal(host(got["counts"]), counts)
+    assert np.array_equal(host(got["offsets"]), offsets)
+    assert np.array_equal(host(got["sorted_src"]), sorted_src)
+    assert np.array_equal(host(got["row_of"]), row_of)
+    # x_perm is a pure copy: bit-exact, checked on the device
+    ref_rows = torch.from_numpy(sorted_src // k).to(DEV)
+    assert torch.equal(got["x_perm"], xd[ref_rows])
+
+
+def test_permute_drops_invalid_ids():
+    say("permute invalid ids")
+    T, d, E, k = 300, 64, 8, 2
+    idx = synth.make_topk_idx(T, E, k, seed=5)
+    idx[10, 1] = -1
+    idx[200, 0] = E
+    xs = np.random.default_rng(1).standard_normal((T, d)).astype(np.float32)
+    got = foe.permute(to_dev(idx, None), to_dev(xs, "f32"), E)
+    valid = (idx >= 0) & (idx < E)
+    counts = np.bincount(idx[valid], minlength=E)
+    assert np.array_equal(host(got["counts"]), counts)
+    off = host(got["offsets"])
+    assert off[-1] == T * k - 2
+    row_of = host(got["row_of"])
+    assert row_of[10 * k + 1] == -1 and row_of[200 * k] == -1
+    flat = idx.ravel()
+    keep = np.nonzero(valid.ravel())[0]
+    order = keep[np.argsort(flat[keep], kind="stable")]
+    assert np.array_equal(host(got["sorted_src"])[: T * k - 2], order)
+
+
+def test_permute_empty_batch():
+    say("permute T=0")
+    got = foe.permute(torch.empty((0, 2), dtype=torch.int32, device=DEV),
+                      torch.empty((0, 64), dtype=torch.bfloat16, device=DEV), 6)
+    assert np.all(host(got["offsets"]) == 0) and np.all(host(got["counts"]) == 0)
+
+
+# ---------------------------------------------------------------------------
+# expert FFN
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("R,E,d,F,empty,dt", [
+    (300, 5, 128, 192, (2,), "bf16"),      # few rows per expert (weight-streaming tiles)
+    (3000, 5, 256, 384, (0,), "bf16"),     # large-tile path, ragged row tails
+    (777, 3, 136, 72, (), "bf16"),         # K and N tails (not multiples of the tiles)
+    (256, 16, 2048, 1024, (), "bf16"),     # decode-shaped
+    (4100, 7, 512, 520, (6,), "bf16"),
+    (128, 4, 128, 256, (), "f32"),
+    (90, 3, 40, 24, (1,), "f32"),
+])
+def test_expert_ffn_parity(R, E, d, F, empty, dt):
+    say("expert_ffn", R, E, d, F, empty, dt)
+    inp = synth.make_ffn_inputs(R, E, d, F, seed=R + d, dtype=dt, empty=empty)
+    y = foe.expert_ffn(to_dev(inp["x_perm"], dt), to_dev(inp["offsets"], None),
+                       to_dev(inp["w_gate"], dt), to_dev(inp["w_up"], dt),
+                       to_dev(inp["w_down"], dt))
+    torch.cuda.synchronize()
+    ref = oracle.expert_ffn(inp["x_perm"], inp["offsets"], inp["w_gate"], inp["w_up"], inp["w_down"])
+    err = rel_err(host(y), ref)
+    say("expert_ffn rel err", err)
+    assert err <= TOL[dt]
+
+
+def test_expert_ffn_prefill_size_sampled():
+    """Full prefill size (rows 16384, d 2048, F 1024, 16 experts, skewed);
+    the oracle recomputes 160 sampled rows."""
+    R, E, d, F = 16384, 16, 2048, 1024
+    say("expert_ffn prefill sampled", R, E, d, F)
+    inp = synth.make_ffn_inputs(R, E, d, F, seed=3, empty=(4,))
+    y = host(foe.expert_ffn(to_dev(inp["x_perm"], "bf16"), to_dev(inp["offsets"], None),
+                            to_dev(inp["w_gate"], "bf16"), to_dev(inp["w_up"], "bf16"),
+                            to_dev(inp["w_down"], "bf16")))
+    off = inp["offsets"]
+    rng = np.random.default_rng(0)
+    rows = np.unique(np.concatenate([np.arange(16), np.arange(R - 16, R), off[:-1].clip(0, R - 1),
+                                     rng.integers(0, R, 112)]))
+    for r in rows:
+        e = int(np.searchsorted(off, r, side="right") - 1)
+        ref = oracle.swiglu_ffn(inp["x_perm"][r:r + 1], inp["w_gate"][e], inp["w_up"][e],
+                                inp["w_down"][e])[0]
+        assert rel_err(y[r], ref) <= 2e-2, (r, e)
+
+
+# ---------------------------------------------------------------------------
+# combine / reduce
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("T,k,d,dt", [(37, 3, 64, "bf16"), (4096, 2, 2048, "bf16"),
+                                      (1000, 4, 136, "f32"), (64, 2, 128, "f32")])
+def test_combine_parity(T, k, d, dt):
+    say("combine", T, k, d, dt)
+    inp = synth.make_combine_inputs(T, k, d, seed=T, dtype=dt)
+    y, row_of, w = to_dev(inp["y_perm"], dt), to_dev(inp["row_of"], None), to_dev(inp["topk_w"], "f32")
+    delta = foe.combine(y, row_of, w)
+    out = foe.combine(y, row_of, w, residual=to_dev(inp["residual"], dt))
+    ref_d = oracle.combine(inp["y_perm"], inp["row_of"], inp["topk_w"])
+    ref_o = oracle.combine(inp["y_perm"], inp["row_of"], inp["topk_w"], inp["residual"])
+    assert rel_err(host(delta), ref_d) <= TOL[dt]
+    assert rel_err(host(out), ref_o) <= TOL[dt]
+
+
+@pytest.mark.parametrize("C,T,d,scale,with_res,dt", [
+    (8, 4096, 2048, 0.125, True, "bf16"), (3, 100, 64, 1.0, False, "bf16"),
+    (1, 33, 8, 0.5, True, "f32"), (5, 64, 128, 0.2, False, "f32")])
+def test_reduce_parity(C, T, d, scale, with_res, dt):
+    say("reduce", C, T, d, scale, with_res, dt)
+    rng = np.random.default_rng(C * T)
+    P = (rng.standard_normal((C, T, d)) * 0.3).astype(np.float32)
+    res = rng.standard_normal((T, d)).astype(np.float32)
+    if dt == "bf16":
+        P, res = synth.round_to_bf16(P), synth.round_to_bf16(res)
+    out = foe.reduce(to_dev(P, dt), scale, residual=to_dev(res, dt) if with_res else None)
+    ref = oracle.reduce_partials(P, scale, res if with_res else None)
+    assert rel_err(host(out), ref) <= TOL[dt]
+
+
+# ---------------------------------------------------------------------------
+# whole block
+# ---------------------------------------------------------------------------
+
+def _block_gpu(inp, reduce_scale=None):
+    cfg = inp["cfg"]
+    w = stacked(inp)
+    out = foe.cluster_block(to_dev(inp["x"], cfg["dtype"]), w["w_router"], w["bias"], w["w_gate"],
+                            w["w_up"], w["w_down"], cfg["k"], reduce_scale=reduce_scale)
+    torch.cuda.synchronize()
+    return host(out)
+
+
+def _block_ref_rows(inp, rows, reduce_scale=None):
+    """Oracle output for the token rows `rows` (per-token formula) and the mask
+    of rows exempt in some cluster."""
+    cfg = inp["cfg"]
+    C = cfg["C"]
+    scale = 1.0 / C if reduce_scale is None else reduce_scale
+    xr = inp["x"][rows].astype(np.float64)
+    acc = np.zeros_like(xr)
+    exempt = np.zeros(len(rows), dtype=bool)
+    for cl in inp["clusters"]:
+        delta, r = oracle.moe_update_tokens(xr, cl, cfg["k"])
+        acc += xr + delta
+        exempt |= r["margin"] < EXEMPT
+    return scale * acc, exempt
+
+
+@pytest.mark.parametrize("name", ["tiny_fp32", "decode_bf16"])
+def test_block_parity_full(name):
+    inp = cfg_inputs(name)
+    cfg = inp["cfg"]
+    say("block full", name)
+    got = _block_gpu(inp)
+    ref, res = oracle.cluster_block(inp["x"], inp["clusters"], cfg["k"])
+    exempt = np.zeros(cfg["T"], dtype=bool)
+    for r in res:
+        exempt |= r["margin"] < EXEMPT
+    keep = ~exempt
+    err = rel_err(got[keep], ref[keep])
+    say("block", name, "rel err", err, "exempt", int(exempt.sum()))
+    assert err <= TOL[cfg["dtype"]]
+
+
+@pytest.mark.parametrize("name", ["prefill_zipf_bf16", "large_bf16", "layer_share_bf16"])
+def test_block_parity_sampled(name):
+    inp = cfg_inputs(name)
+    cfg = inp["cfg"]
+    T = cfg["T"]
+    say("block sampled", name, "T", T, "C", cfg["C"])
+    got = _block_gpu(inp)
+    rng = np.random.default_rng(1)
+    rows = np.unique(np.concatenate([np.arange(24), np.arange(T - 24, T), rng.integers(0, T, 80)]))
+    ref, exempt = _block_ref_rows(inp, rows)
+    keep = ~exempt
+    err = rel_err(got[rows][keep], ref[keep])
+    say("block", name, "rel err", err, "exempt", int(exempt.sum()))
+    assert err <= 2e-2
+    assert np.all(np.isfinite(got))
+
+
+@pytest.mark.parametrize("T,d,E,k,F,C,scale,dt,bias", [
+    (1000, 256, 8, 2, 384, 1, None, "bf16", None),   # large tiles, ragged tails
+    (100, 256, 16, 2, 128, 1, None, "bf16", None),   # small-row tiles
+    (50, 64, 4, 4, 64, 1, None, "bf16", None),       # k = E (dense mixture)
+    (33, 32, 1, 1, 48, 1, None, "f32", None),        # E = 1, k = 1
+    (1, 64, 8, 2, 64, 3, 1.0, "bf16", None),         # one token, literal sum of 3
+    (257, 128, 8, 2, 128, 2, None, "bf16", "zipf4"),  # extreme skew: empty experts
+    (130, 64, 4, 2, 64, 2, 0.5, "f32", None),
+])
+def test_block_parity_shapes(T, d, E, k, F, C, scale, dt, bias):
+    say("block shapes", T, d, E, k, F, C, scale, dt, bias)
+    cfg = dict(dtype=dt, C=C, T=T, d=d, E=E, k=k, F=F, sigma=0.05, seed=T + d, bias=bias)
+    inp = synth.make_block_inputs(cfg)
+    got = _block_gpu(inp, scale)
+    ref, res = oracle.cluster_block(inp["x"], inp["clusters"], k, scale)
+    exempt = np.zeros(T, dtype=bool)
+    for r in res:
+        exempt |= r["margin"] < EXEMPT
+    assert rel_err(got[~exempt], ref[~exempt]) <= TOL[dt]
+
+
+def test_block_is_deterministic():
+    inp = cfg_inputs("decode_bf16")
+    say("block determinism")
+    a = _block_gpu(inp)
+    b = _block_gpu(inp)
+    assert np.array_equal(a, b)
+
+
+def test_pipeline_properties_at_prefill_size():
+    """Properties that hold at any size, on the real prefill configuration:
+    every permuted row holds its expert's token, segments ascend, the counts
+    sum to T*k, and combine(y = x_perm) with unit weights gives k * x."""
+    inp = cfg_inputs("prefill_zipf_bf16")
+    cfg = inp["cfg"]
+    T, k, E = cfg["T"], cfg["k"], cfg["E"]
+    say("properties prefill")
+    cl = inp["clusters"][0]
+    x = to_dev(inp["x"], "bf16")
+    idx, w = foe.route(x, to_dev(cl["w_router"], "bf16"), to_dev(cl["bias"], "f32"), k)
+    p = foe.permute(idx, x, E)
+    counts = host(p["counts"])
+    assert counts.sum() == T * k and counts.max() > 4 * np.median(counts)  # Zipf skew
+    src = host(p["sorted_src"]).astype(np.int64)
+    assert np.array_equal(np.sort(src), np.arange(T * k))
+    flat = host(idx).ravel()
+    off = host(p["offsets"])
+    for e in range(E):
+        seg = src[off[e]:off[e + 1]]
+        assert np.all(flat[seg] == e) and np.all(np.diff(seg) > 0)
+    ones = torch.ones((T, k), dtype=torch.float32, device=DEV)
+    back = foe.combine(p["x_perm"], p["row_of"], ones)
+    assert torch.equal(back.float(), (x.float() * k).bfloat16().float())
+
+
+def test_block_graph_replay_matches_eager():
+    """The block captured in a HIP graph: every replay (with eager work and
+    synchronisations in between) equals the eager result bit for bit."""
+    inp = cfg_inputs("decode_bf16")
+    cfg = inp["cfg"]
+    say("block graph replay")
+    w = stacked(inp)
+    x = to_dev(inp["x"], "bf16")
+    C, T, d, E, k, F = cfg["C"], cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["F"]
+    ws = torch.empty(foe.workspace_bytes("cluster_block", foe.BF16, C, T, d, E, k, F),
+                     dtype=torch.uint8, device=DEV)
+    out = torch.empty((T, d), dtype=torch.bfloat16, device=DEV)
+    eager = foe.cluster_block(x, w["w_router"], w["bias"], w["w_gate"], w["w_up"], w["w_down"], k,
+                              ws=ws).clone()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    with torch.cuda.graph(g, stream=side):
+        foe.cluster_block(x, w["w_router"], w["bias"], w["w_gate"], w["w_up"], w["w_down"], k,
+                          out=out, ws=ws, stream=side)
+    for rep in range(4):
+        out.fill_(0)
+        ws.fill_(7)  # scribble over the workspace between replays
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), rep
+        # unrelated eager work in between
+        foe.route(x, w["w_router"][0], None, k)
+        torch.cuda.synchronize()
