@@ -48,7 +48,9 @@ def _run(cmd):
     return p.returncode, "\n".join(lines)
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, extra_flags=(), out_path: str = LIB_PATH) -> str:
+    """Compile every source and link ``out_path`` (default: the in-tree library).
+    ``extra_flags`` are appended to each compile line (e.g. ``-D`` tile macros)."""
     hipcc = _hipcc()
     with tempfile.TemporaryDirectory(prefix="foe_build_") as tmp:
         objs = []
@@ -56,7 +58,7 @@ def build(verbose: bool = False) -> str:
         for src in SOURCES:
             obj = os.path.join(tmp, src.replace(".hip", ".o"))
             objs.append(obj)
-            cmds.append([hipcc, *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c",
+            cmds.append([hipcc, *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, "-I", CSRC, "-c",
                          os.path.join(CSRC, src), "-o", obj])
         jobs = min(len(cmds), int(os.environ.get("MAX_JOBS", "8")))
         with ThreadPoolExecutor(max_workers=jobs) as ex:
@@ -70,10 +72,10 @@ def build(verbose: bool = False) -> str:
         rc, out = _run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp_lib, *objs])
         if rc != 0:
             raise RuntimeError(f"link failed ({rc}):\n{out}")
-        staged = LIB_PATH + ".tmp"
+        staged = out_path + ".tmp"
         shutil.copyfile(tmp_lib, staged)
-        os.replace(staged, LIB_PATH)
-    return LIB_PATH
+        os.replace(staged, out_path)
+    return out_path
 
 
 if __name__ == "__main__":

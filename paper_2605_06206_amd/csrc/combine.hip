@@ -14,33 +14,52 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
                                                       const T* __restrict__ res, int T_, int d,
                                                       int k, T* __restrict__ out) {
   constexpr int EPV = Vec16<T>::N;
-  constexpr int U = 2;  // row chunks per lane in flight
+  constexpr int U = 4;  // row chunks per lane; two slots' gathers are in flight together
   const int lane = lane_id();
   const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (tok >= T_) return;
   const int R = T_ * k;
   const int nvec = d / EPV;
+  const int32_t* rows = row_of + (size_t)tok * k;
+  const float* wts = w + (size_t)tok * k;
   for (int c0 = 0; c0 < nvec; c0 += U * kWave) {
     float acc[U][EPV];
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int v = 0; v < EPV; ++v) acc[u][v] = 0.f;
-    for (int j = 0; j < k; ++j) {
-      const int p = row_of[(size_t)tok * k + j];
-      const float wj = w[(size_t)tok * k + j];
-      if (p < 0 || p >= R) continue;
-      const T* src = y + (size_t)p * d;
-      Vec16<T> v[U];
+    Vec16<T> res_v[U];
+    if (res != nullptr) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int c = c0 + u * kWave + lane;
-        if (c < nvec) v[u] = load16_cached(src + (size_t)c * EPV);
+        if (c < nvec) res_v[u] = load16_cached(res + (size_t)tok * d + (size_t)c * EPV);
+      }
+    }
+    for (int j = 0; j < k; j += 2) {
+      // slots j and j+1 (the second may be absent); summed in slot order
+      const bool two = j + 1 < k;
+      const int p0 = rows[j], p1 = two ? rows[j + 1] : -1;
+      const float w0 = wts[j], w1 = two ? wts[j + 1] : 0.f;
+      const bool ok0 = p0 >= 0 && p0 < R, ok1 = p1 >= 0 && p1 < R;
+      Vec16<T> v0[U], v1[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c = c0 + u * kWave + lane;
+        if (c < nvec && ok0) v0[u] = load16_cached(y + (size_t)p0 * d + (size_t)c * EPV);
+        if (c < nvec && ok1) v1[u] = load16_cached(y + (size_t)p1 * d + (size_t)c * EPV);
       }
 #pragma unroll
-      for (int u = 0; u < U; ++u)
+      for (int u = 0; u < U; ++u) {
+        if (ok0) {
 #pragma unroll
-        for (int e = 0; e < EPV; ++e) acc[u][e] = fmaf(wj, to_f32(v[u].v[e]), acc[u][e]);
+          for (int e = 0; e < EPV; ++e) acc[u][e] = fmaf(w0, to_f32(v0[u].v[e]), acc[u][e]);
+        }
+        if (ok1) {
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) acc[u][e] = fmaf(w1, to_f32(v1[u].v[e]), acc[u][e]);
+        }
+      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -48,9 +67,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
       if (c >= nvec) continue;
       Vec16<T> o;
       if (res != nullptr) {
-        Vec16<T> r = load16_cached(res + (size_t)tok * d + (size_t)c * EPV);
 #pragma unroll
-        for (int e = 0; e < EPV; ++e) o.v[e] = from_f32<T>(to_f32(r.v[e]) + acc[u][e]);
+        for (int e = 0; e < EPV; ++e) o.v[e] = from_f32<T>(to_f32(res_v[u].v[e]) + acc[u][e]);
       } else {
 #pragma unroll
         for (int e = 0; e < EPV; ++e) o.v[e] = from_f32<T>(acc[u][e]);

@@ -13,8 +13,41 @@
 // sum over the per-expert tile counts, so no host sync is needed.
 #include "foe_common.hpp"
 
+// Tile shapes (BM, BN per weight matrix, BK, waves along M, waves along N).
+// Large tiles when experts receive many rows (MFMA-bound), small ones when
+// they receive few (weight-streaming bound).
+#ifndef FOE_PRE_GU
+#define FOE_PRE_GU 256, 128, 64, 2, 2
+#endif
+#ifndef FOE_PRE_DN
+#define FOE_PRE_DN 256, 256, 64, 2, 2
+#endif
+#ifndef FOE_PRE_OCC
+#define FOE_PRE_OCC 1
+#endif
+#ifndef FOE_PIPE_GU
+#define FOE_PIPE_GU 256, 128, 2, 4
+#endif
+#ifndef FOE_PIPE_DN
+#define FOE_PIPE_DN 256, 256, 2, 4
+#endif
+#ifndef FOE_PIPE_OPT
+#define FOE_PIPE_OPT 1, 2
+#endif
+#ifndef FOE_SKINNY
+#define FOE_SKINNY 4, 4
+#endif
+#ifndef FOE_DEC_GU
+#define FOE_DEC_GU 32, 64, 64, 1, 2
+#endif
+#ifndef FOE_DEC_DN
+#define FOE_DEC_DN 32, 64, 64, 1, 2
+#endif
+
 namespace foe {
 namespace {
+
+template <int W, int U> struct GemmWaves { static constexpr int value = W; };
 
 // Find the (expert, first row, row end) of global M-tile `mt`.  Returns false
 // if `mt` is past the last tile.  Offsets are clamped to [0, rows]; a
@@ -65,6 +98,7 @@ __device__ bool find_tile(const int32_t* __restrict__ offsets, int E, int rows, 
   return true;
 }
 
+constexpr int kSkinnyWaves = GemmWaves<FOE_SKINNY>::value;
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
 template <int BM, int BN, int BK, int WM, int WN, bool GATEUP>
@@ -84,16 +118,38 @@ struct GemmCfg {
   static_assert(BM * CPR % NTHR == 0 && BN * CPR % NTHR == 0, "even load split");
 };
 
-template <int BM, int BN, int BK, int WM, int WN, bool GATEUP>
-__global__ __launch_bounds__(WM* WN* kWave) void grouped_gemm_bf16(
+// Workgroups are dealt round-robin to the 8 XCDs (each with its own L2).  The
+// tile index is remapped so that each XCD walks a contiguous range of tiles:
+// neighbouring tiles share their A rows (same M-tile) or their weight slice
+// (same expert), and now meet in the same L2.
+__device__ __forceinline__ int xcd_tile(int bid, int nblocks) {
+  constexpr int kXcd = 8;
+  const int per = (nblocks + kXcd - 1) / kXcd;
+  return (bid % kXcd) * per + bid / kXcd;
+}
+
+// Buffer resource over `nbytes` bytes from `base`: loads at offsets at or past
+// `nbytes` return zeros, which handles ragged rows and K tails without branches.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nbytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+template <int BM, int BN, int BK, int WM, int WN, bool GATEUP, int MAXW>
+__global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1, MAXW)))
+void grouped_gemm_bf16(
     const bf16* __restrict__ A, const int32_t* __restrict__ offsets, int E, int rows,
     const bf16* __restrict__ B0, const bf16* __restrict__ B1, int N, int K,
-    bf16* __restrict__ out, int n_tiles_n) {
+    bf16* __restrict__ out, int n_tiles_n, int n_tiles) {
   using C = GemmCfg<BM, BN, BK, WM, WN, GATEUP>;
   __shared__ __align__(16) bf16 lds[2 * C::STAGE_ELEMS];
 
-  const int mt = blockIdx.x / n_tiles_n;
-  const int ntile = blockIdx.x % n_tiles_n;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  if (tile >= n_tiles) return;
+  const int mt = tile / n_tiles_n;
+  const int ntile = tile % n_tiles_n;
   int e, row0, row_end;
   if (!find_tile(offsets, E, rows, BM, mt, e, row0, row_end)) return;
   const int n0 = ntile * BN;
@@ -103,9 +159,35 @@ __global__ __launch_bounds__(WM* WN* kWave) void grouped_gemm_bf16(
   const int wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
 
-  const bf16* Bw[2];
-  Bw[0] = B0 + (size_t)e * N * K;
-  Bw[1] = GATEUP ? B1 + (size_t)e * N * K : nullptr;
+  // one buffer per operand tile: BM rows of A, BN rows of each weight matrix
+  const int m_valid = min(BM, row_end - row0);
+  const int n_valid = min(BN, N - n0);
+  const __amdgpu_buffer_rsrc_t ra_rsrc =
+      make_rsrc(A + (size_t)row0 * K, (uint32_t)m_valid * K * 2u);
+  __amdgpu_buffer_rsrc_t rb_rsrc[C::NB];
+  rb_rsrc[0] = make_rsrc(B0 + ((size_t)e * N + n0) * K, (uint32_t)n_valid * K * 2u);
+  if constexpr (GATEUP) rb_rsrc[C::NB - 1] = make_rsrc(B1 + ((size_t)e * N + n0) * K, (uint32_t)n_valid * K * 2u);
+
+  // per-thread byte offsets of its 16-byte chunks inside a K-slab; LDS slots
+  uint32_t a_off[C::A_PER], b_off[C::B_PER];
+  int a_kc[C::A_PER], b_kc[C::B_PER];
+  int a_lds[C::A_PER], b_lds[C::B_PER];
+#pragma unroll
+  for (int i = 0; i < C::A_PER; ++i) {
+    const int c = tid + i * C::NTHR;
+    const int r = c / C::CPR, kc = c % C::CPR;
+    a_off[i] = (uint32_t)(r * K + kc * 8) * 2u;
+    a_kc[i] = kc * 8;
+    a_lds[i] = r * C::LDK + kc * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < C::B_PER; ++i) {
+    const int c = tid + i * C::NTHR;
+    const int r = c / C::CPR, kc = c % C::CPR;
+    b_off[i] = (uint32_t)(r * K + kc * 8) * 2u;
+    b_kc[i] = kc * 8;
+    b_lds[i] = r * C::LDK + kc * 8;
+  }
 
   f32x16 acc[C::NB][C::SM][C::SN];
 #pragma unroll
@@ -119,47 +201,49 @@ __global__ __launch_bounds__(WM* WN* kWave) void grouped_gemm_bf16(
 
   u32x4 ra[C::A_PER];
   u32x4 rb[C::NB][C::B_PER];
+  constexpr uint32_t kOob = 0x80000000u;  // past any tile buffer: reads zeros
 
   auto gload = [&](int k0) {
+    const uint32_t kb = (uint32_t)k0 * 2u;
 #pragma unroll
-    for (int i = 0; i < C::A_PER; ++i) {
-      const int c = tid + i * C::NTHR;
-      const int r = c / C::CPR, kc = c % C::CPR;
-      const int gr = row0 + r, gk = k0 + kc * 8;
-      ra[i] = (gr < row_end && gk < K)
-                  ? *reinterpret_cast<const u32x4*>(A + (size_t)gr * K + gk)
-                  : zero_u32x4();
-    }
+    for (int i = 0; i < C::A_PER; ++i)
+      ra[i] = buf_load16(ra_rsrc, (k0 + a_kc[i] < K) ? a_off[i] + kb : kOob);
 #pragma unroll
     for (int b = 0; b < C::NB; ++b)
 #pragma unroll
-      for (int i = 0; i < C::B_PER; ++i) {
-        const int c = tid + i * C::NTHR;
-        const int r = c / C::CPR, kc = c % C::CPR;
-        const int gn = n0 + r, gk = k0 + kc * 8;
-        rb[b][i] = (gn < N && gk < K)
-                       ? *reinterpret_cast<const u32x4*>(Bw[b] + (size_t)gn * K + gk)
-                       : zero_u32x4();
-      }
+      for (int i = 0; i < C::B_PER; ++i)
+        rb[b][i] = buf_load16(rb_rsrc[b], (k0 + b_kc[i] < K) ? b_off[i] + kb : kOob);
   };
   auto lstore = [&](int buf) {
     bf16* sa = lds + buf * C::STAGE_ELEMS;
 #pragma unroll
-    for (int i = 0; i < C::A_PER; ++i) {
-      const int c = tid + i * C::NTHR;
-      const int r = c / C::CPR, kc = c % C::CPR;
-      *reinterpret_cast<u32x4*>(sa + r * C::LDK + kc * 8) = ra[i];
-    }
+    for (int i = 0; i < C::A_PER; ++i) *reinterpret_cast<u32x4*>(sa + a_lds[i]) = ra[i];
 #pragma unroll
     for (int b = 0; b < C::NB; ++b) {
       bf16* sb = sa + C::A_ELEMS + b * C::B_ELEMS;
 #pragma unroll
-      for (int i = 0; i < C::B_PER; ++i) {
-        const int c = tid + i * C::NTHR;
-        const int r = c / C::CPR, kc = c % C::CPR;
-        *reinterpret_cast<u32x4*>(sb + r * C::LDK + kc * 8) = rb[b][i];
-      }
+      for (int i = 0; i < C::B_PER; ++i) *reinterpret_cast<u32x4*>(sb + b_lds[i]) = rb[b][i];
     }
+  };
+
+  // fragment addresses (elements) inside a stage
+  const int lrow = lane & 31;
+  const int lk = (lane >> 5) * 8;
+  const int xa_base = (wm * C::WTM + lrow) * C::LDK + lk;
+  const int wf_base = C::A_ELEMS + (wn * C::WTN + lrow) * C::LDK + lk;
+
+  bf16x8 xa[2][C::SM];
+  bf16x8 wf[2][C::NB][C::SN];
+  auto fload = [&](const bf16* sa, int kk, int slot) {
+#pragma unroll
+    for (int i = 0; i < C::SM; ++i)
+      xa[slot][i] = *reinterpret_cast<const bf16x8*>(sa + xa_base + i * 32 * C::LDK + kk);
+#pragma unroll
+    for (int b = 0; b < C::NB; ++b)
+#pragma unroll
+      for (int j = 0; j < C::SN; ++j)
+        wf[slot][b][j] = *reinterpret_cast<const bf16x8*>(sa + wf_base + b * C::B_ELEMS +
+                                                          j * 32 * C::LDK + kk);
   };
 
   const int nk = (K + BK - 1) / BK;
@@ -167,30 +251,29 @@ __global__ __launch_bounds__(WM* WN* kWave) void grouped_gemm_bf16(
   lstore(0);
   __syncthreads();
 
-  const int lrow = lane & 31;
-  const int lk = (lane >> 5) * 8;
+  // The scheduling barriers pin the pipeline the compiler would otherwise
+  // undo: next stage's global loads first, then for every k16 step the LDS
+  // reads of the next fragments are issued before the MFMAs of the current.
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
     if (kt + 1 < nk) gload((kt + 1) * BK);
     const bf16* sa = lds + buf * C::STAGE_ELEMS;
+    fload(sa, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 16) {
-      bf16x8 xa[C::SM];
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int cur = ks & 1;
+      if (ks + 1 < BK / 16) fload(sa, (ks + 1) * 16, cur ^ 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < C::SM; ++i)
-        xa[i] = *reinterpret_cast<const bf16x8*>(sa + (wm * C::WTM + i * 32 + lrow) * C::LDK + kk + lk);
+      for (int b = 0; b < C::NB; ++b)
 #pragma unroll
-      for (int b = 0; b < C::NB; ++b) {
-        const bf16* sb = sa + C::A_ELEMS + b * C::B_ELEMS;
-#pragma unroll
-        for (int j = 0; j < C::SN; ++j) {
-          const bf16x8 wf =
-              *reinterpret_cast<const bf16x8*>(sb + (wn * C::WTN + j * 32 + lrow) * C::LDK + kk + lk);
+        for (int j = 0; j < C::SN; ++j)
 #pragma unroll
           for (int i = 0; i < C::SM; ++i)
-            acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, xa[i], acc[b][i][j], 0, 0, 0);
-        }
-      }
+            acc[b][i][j] =
+                __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cur][b][j], xa[cur][i], acc[b][i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
     if (kt + 1 < nk) lstore(buf ^ 1);
     __syncthreads();
@@ -217,6 +300,343 @@ __global__ __launch_bounds__(WM* WN* kWave) void grouped_gemm_bf16(
         *reinterpret_cast<bf16x4*>(out + (size_t)m * N + n) = o;
       }
     }
+  }
+}
+
+// LDS-only workgroup barrier: waits for this wave's LDS operations and meets
+// the other waves, but (unlike __syncthreads) does not drain outstanding
+// global loads, so prefetches stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Scheduling-group masks of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008, kSchedDsRead = 0x100, kSchedDsWrite = 0x200,
+              kSchedVmemRead = 0x020;
+
+// Ask the scheduler for the order  MFMA, LDS read, <share of X>, MFMA, ...
+// over one k16 step: NM MFMAs, NR fragment reads and NX extra instructions of
+// kind XMASK spread evenly after the reads.  A single wave per SIMD issues in
+// order, so a burst of memory instructions would otherwise idle its MFMA pipe.
+template <int I, int NM, int NR, int NX, int XMASK>
+__device__ __forceinline__ void interleave() {
+  if constexpr (I < NM) {
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+    if constexpr (I < NR) {
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+      constexpr int per = (NX + NR - 1) / NR;
+      constexpr int done = I * per;
+      constexpr int n = (NX - done) < per ? (NX - done) : per;
+      if constexpr (n > 0) __builtin_amdgcn_sched_group_barrier(XMASK, n, 0);
+    }
+    interleave<I + 1, NM, NR, NX, XMASK>();
+  }
+}
+
+// Large-M grouped GEMM: BK = 64, two LDS stages, two register staging sets.
+// A stage is loaded from global memory two iterations before it is written to
+// LDS, so about two stages of loads (≈ 1.5 iterations of MFMA time) are in
+// flight at any moment.  Per iteration (4 k16 steps of 16-32 MFMAs):
+//   ks0: read frags ks1; MFMA ks0; write staged stage kt+1 to the other LDS
+//        buffer
+//   ks1: read frags ks2; MFMA ks1; issue global loads of stage kt+3
+//   ks2: read frags ks3; MFMA ks2; LDS barrier (stage kt+1 complete, and every
+//        wave is done reading stage kt's buffer except registers)
+//   ks3: read frags ks0 of stage kt+1; MFMA ks3
+template <int BM, int BN, int WM, int WN, bool GATEUP, int NSETS, int MAXW>
+__global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1, MAXW)))
+void grouped_gemm_bf16_pipe(
+    const bf16* __restrict__ A, const int32_t* __restrict__ offsets, int E, int rows,
+    const bf16* __restrict__ B0, const bf16* __restrict__ B1, int N, int K,
+    bf16* __restrict__ out, int n_tiles_n, int n_tiles) {
+  constexpr int BK = 64;
+  using C = GemmCfg<BM, BN, BK, WM, WN, GATEUP>;
+  constexpr int NLD = C::A_PER + C::NB * C::B_PER;  // 16-byte loads per thread per stage
+  // two separate arrays so the compiler can tell the stages apart (the stage
+  // index is a compile-time constant in the unrolled loop)
+  __shared__ __align__(16) bf16 lds0[C::STAGE_ELEMS];
+  __shared__ __align__(16) bf16 lds1[C::STAGE_ELEMS];
+  auto stage = [&](int b) -> bf16* { return b ? lds1 : lds0; };
+
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  if (tile >= n_tiles) return;
+  const int mt = tile / n_tiles_n;
+  const int ntile = tile % n_tiles_n;
+  int e, row0, row_end;
+  if (!find_tile(offsets, E, rows, BM, mt, e, row0, row_end)) return;
+  const int n0 = ntile * BN;
+
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+
+  const int m_valid = min(BM, row_end - row0);
+  const int n_valid = min(BN, N - n0);
+  __amdgpu_buffer_rsrc_t rsrc[1 + C::NB];
+  rsrc[0] = make_rsrc(A + (size_t)row0 * K, (uint32_t)m_valid * K * 2u);
+  rsrc[1] = make_rsrc(B0 + ((size_t)e * N + n0) * K, (uint32_t)n_valid * K * 2u);
+  if constexpr (GATEUP) rsrc[2] = make_rsrc(B1 + ((size_t)e * N + n0) * K, (uint32_t)n_valid * K * 2u);
+
+  // chunk i of a stage: operand, byte offset in the K-slab, k of the chunk, LDS slot
+  uint32_t g_off[NLD];
+  int g_k[NLD], l_off[NLD];
+#pragma unroll
+  for (int i = 0; i < NLD; ++i) {
+    int c, rows_before, base;
+    if (i < C::A_PER) {
+      c = tid + i * C::NTHR;
+      base = 0;
+      rows_before = 0;
+    } else {
+      const int j = i - C::A_PER;
+      const int b = j / C::B_PER;
+      c = tid + (j % C::B_PER) * C::NTHR;
+      base = C::A_ELEMS + b * C::B_ELEMS;
+      rows_before = 0;
+    }
+    (void)rows_before;
+    const int r = c / C::CPR, kc = c % C::CPR;
+    g_off[i] = (uint32_t)(r * K + kc * 8) * 2u;
+    g_k[i] = kc * 8;
+    l_off[i] = base + r * C::LDK + kc * 8;
+  }
+  auto rsrc_of = [&](int i) {
+    return i < C::A_PER ? rsrc[0] : rsrc[1 + (i - C::A_PER) / C::B_PER];
+  };
+
+  f32x16 acc[C::NB][C::SM][C::SN];
+#pragma unroll
+  for (int b = 0; b < C::NB; ++b)
+#pragma unroll
+    for (int i = 0; i < C::SM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::SN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[b][i][j][v] = 0.f;
+
+  u32x4 stg[NSETS][NLD];
+  constexpr uint32_t kOob = 0x80000000u;
+  auto gload = [&](int set, int k0) {
+    const uint32_t kb = (uint32_t)k0 * 2u;
+#pragma unroll
+    for (int i = 0; i < NLD; ++i)
+      stg[set][i] = buf_load16(rsrc_of(i), (k0 + g_k[i] < K) ? g_off[i] + kb : kOob);
+  };
+  auto lstore = [&](int set, int buf) {
+    bf16* sb = stage(buf);
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) *reinterpret_cast<u32x4*>(sb + l_off[i]) = stg[set][i];
+  };
+
+  const int lrow = lane & 31;
+  const int lk = (lane >> 5) * 8;
+  const int xa_base = (wm * C::WTM + lrow) * C::LDK + lk;
+  const int wf_base = C::A_ELEMS + (wn * C::WTN + lrow) * C::LDK + lk;
+  bf16x8 xa[2][C::SM];
+  bf16x8 wf[2][C::NB][C::SN];
+  auto fload = [&](int buf, int ks, int slot) {
+    const bf16* sa = stage(buf) + ks * 16;
+#pragma unroll
+    for (int i = 0; i < C::SM; ++i)
+      xa[slot][i] = *reinterpret_cast<const bf16x8*>(sa + xa_base + i * 32 * C::LDK);
+#pragma unroll
+    for (int b = 0; b < C::NB; ++b)
+#pragma unroll
+      for (int j = 0; j < C::SN; ++j)
+        wf[slot][b][j] =
+            *reinterpret_cast<const bf16x8*>(sa + wf_base + b * C::B_ELEMS + j * 32 * C::LDK);
+  };
+  auto mfma = [&](int slot) {
+#pragma unroll
+    for (int b = 0; b < C::NB; ++b)
+#pragma unroll
+      for (int j = 0; j < C::SN; ++j)
+#pragma unroll
+        for (int i = 0; i < C::SM; ++i)
+          acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[slot][b][j], xa[slot][i],
+                                                                 acc[b][i][j], 0, 0, 0);
+  };
+  constexpr int NM = C::NB * C::SM * C::SN;  // MFMAs per k16 step
+  constexpr int NR = C::SM + C::NB * C::SN;  // fragment reads per k16 step
+  // stage s is staged in register set s % NSETS; at iteration kt the set of
+  // stage kt+1 is written to LDS and then refilled with stage kt+1+NSETS
+  auto iteration = [&](int kt, int cur) {
+    const int nxt = cur ^ 1;
+    const int set = (kt + 1) % NSETS;
+    fload(cur, 1, 1);
+    mfma(0);
+    lstore(set, nxt);
+    interleave<0, NM, NR, NLD, kSchedDsWrite>();
+    __builtin_amdgcn_sched_barrier(0);
+    fload(cur, 2, 0);
+    mfma(1);
+    gload(set, (kt + 1 + NSETS) * BK);
+    interleave<0, NM, NR, NLD, kSchedVmemRead>();
+    __builtin_amdgcn_sched_barrier(0);
+    fload(cur, 3, 1);
+    mfma(0);
+    interleave<0, NM, NR, 0, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    lds_barrier();
+    fload(nxt, 0, 0);
+    mfma(1);
+    interleave<0, NM, NR, 0, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // K steps rounded up to an even count: steps past K read zeros
+  const int nk = ((K + BK - 1) / BK + 1) & ~1;
+#pragma unroll
+  for (int st = 0; st < NSETS; ++st) gload(st, st * BK);
+  lstore(0, 0);
+  gload(0, NSETS * BK);
+  lds_barrier();
+  fload(0, 0, 0);
+  for (int kt = 0; kt < nk; kt += 2) {
+    iteration(kt, 0);
+    iteration(kt + 1, 1);
+  }
+
+#pragma unroll
+  for (int i = 0; i < C::SM; ++i) {
+    const int m = row0 + wm * C::WTM + i * 32 + lrow;
+    if (m >= row_end) continue;
+#pragma unroll
+    for (int j = 0; j < C::SN; ++j) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = n0 + wn * C::WTN + j * 32 + q * 8 + (lane >> 5) * 4;
+        if (n >= N) continue;
+        bf16x4 o;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          float val = acc[0][i][j][q * 4 + v];
+          if constexpr (GATEUP) val = silu_f(val) * acc[C::NB - 1][i][j][q * 4 + v];
+          o[v] = (bf16)val;
+        }
+        *reinterpret_cast<bf16x4*>(out + (size_t)m * N + n) = o;
+      }
+    }
+  }
+}
+
+// Few rows per expert (decode): the FFN is a weight stream.  A workgroup owns
+// one expert and a slice of weight rows (16 gate + 16 up rows, or 32 down
+// rows); its 4 waves split K and read the weights with 128-bit buffer loads
+// straight into the operands of v_mfma_f32_16x16x32_bf16 (D = W * X^T, 16
+// weight rows x 16 token rows per MFMA), so there is no LDS staging and every
+// wave keeps several K chunks of loads in flight.  The 4 partial tiles are
+// summed in LDS in wave order.  Experts with more than 32 rows take several
+// passes over their rows.
+template <bool GATEUP, int kWavesK, int U>
+__global__ __launch_bounds__(kWavesK * 64) void ffn_skinny_bf16(
+    const bf16* __restrict__ X, const int32_t* __restrict__ offsets, int E, int rows,
+    const bf16* __restrict__ W0, const bf16* __restrict__ W1, int N, int K,
+    bf16* __restrict__ out, int n_groups) {
+  // kWavesK waves split K; each issues the loads of U K chunks (of 32) at once
+  constexpr int NPB = GATEUP ? 16 : 32;  // output columns per workgroup
+  __shared__ __align__(16) f32x4 red[kWavesK][2][2][kWave];
+
+  const int e = blockIdx.x / n_groups;
+  const int n0 = (blockIdx.x % n_groups) * NPB;
+  const int a = min(max(offsets[e], 0), rows);
+  const int b = max(min(max(offsets[e + 1], 0), rows), a);
+  if (b == a || e >= E) return;
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int r16 = lane & 15;
+  const uint32_t kq = (uint32_t)(lane >> 4) * 8u;
+
+  // weight tiles: tile 0 / tile 1 = gate / up rows n0.. (GATEUP) or rows n0.., n0+16..
+  const int nv = min(NPB, N - n0);
+  __amdgpu_buffer_rsrc_t wr0, wr1;
+  if constexpr (GATEUP) {
+    wr0 = make_rsrc(W0 + ((size_t)e * N + n0) * K, (uint32_t)nv * K * 2u);
+    wr1 = make_rsrc(W1 + ((size_t)e * N + n0) * K, (uint32_t)nv * K * 2u);
+  } else {
+    wr0 = make_rsrc(W0 + ((size_t)e * N + n0) * K, (uint32_t)nv * K * 2u);
+    wr1 = wr0;
+  }
+  const uint32_t w_off0 = (uint32_t)r16 * K * 2u + kq * 2u;
+  const uint32_t w_off1 = GATEUP ? w_off0 : (uint32_t)(r16 + 16) * K * 2u + kq * 2u;
+  const int nchunks = (K + 31) / 32;
+  constexpr uint32_t kOob = 0x80000000u;
+
+  for (int t0 = a; t0 < b; t0 += 32) {
+    const int tv = min(32, b - t0);
+    const __amdgpu_buffer_rsrc_t xr = make_rsrc(X + (size_t)t0 * K, (uint32_t)tv * K * 2u);
+    const uint32_t x_off0 = (uint32_t)r16 * K * 2u + kq * 2u;
+    const uint32_t x_off1 = (uint32_t)(r16 + 16) * K * 2u + kq * 2u;
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c0 = wave * U; c0 < nchunks; c0 += kWavesK * U) {
+      u32x4 wa[U][2], xb[U][2];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c = c0 + u;
+        const bool ok = c < nchunks && (uint32_t)c * 32u + kq < (uint32_t)K;
+        const uint32_t kb = (uint32_t)c * 64u;
+        wa[u][0] = buf_load16(wr0, ok ? w_off0 + kb : kOob);
+        wa[u][1] = buf_load16(wr1, ok ? w_off1 + kb : kOob);
+        xb[u][0] = buf_load16(xr, ok ? x_off0 + kb : kOob);
+        xb[u][1] = buf_load16(xr, (ok && tv > 16) ? x_off1 + kb : kOob);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, wa[u][i]), __builtin_bit_cast(bf16x8, xb[u][j]),
+                acc[i][j], 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) red[wave][i][j][lane] = acc[i][j];
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          f32x4 s4 = red[0][i][j][lane];
+#pragma unroll
+          for (int w = 1; w < kWavesK; ++w) s4 += red[w][i][j][lane];
+          acc[i][j] = s4;
+        }
+      // lane holds token j*16 + lane%16 and weight rows 4*(lane/16) + [0,4)
+      const int nb = 4 * (lane >> 4);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int tok = j * 16 + r16;
+        if (tok >= tv) continue;
+        bf16* orow = out + (size_t)(t0 + tok) * N + n0;
+        if constexpr (GATEUP) {
+          if (nb < nv) {
+            bf16x4 o;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) o[v] = (bf16)(silu_f(acc[0][j][v]) * acc[1][j][v]);
+            *reinterpret_cast<bf16x4*>(orow + nb) = o;
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            if (i * 16 + nb >= nv) continue;
+            bf16x4 o;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) o[v] = (bf16)acc[i][j][v];
+            *reinterpret_cast<bf16x4*>(orow + i * 16 + nb) = o;
+          }
+        }
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -267,15 +687,30 @@ __global__ __launch_bounds__(256) void down_f32(const float* __restrict__ h,
   y[(size_t)row * d + c] = acc;
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool GATEUP>
+template <int BM, int BN, int BK, int WM, int WN, bool GATEUP, int MAXW>
 void launch_gemm(const bf16* A, const int32_t* offsets, int E, int rows, const bf16* B0,
                  const bf16* B1, int N, int K, bf16* out, hipStream_t s, const char* name) {
   const int ntn = ceil_div(N, BN);
   const int max_mt = ceil_div(rows, BM) + E;  // sum_e ceil(M_e/BM) <= rows/BM + E
-  dim3 grid((unsigned)((long long)max_mt * ntn));
+  const long long n_tiles = (long long)max_mt * ntn;
+  dim3 grid((unsigned)((n_tiles + 7) / 8 * 8));
   ProfileScope ps(name, s);
-  hipLaunchKernelGGL((grouped_gemm_bf16<BM, BN, BK, WM, WN, GATEUP>), grid, dim3(WM * WN * kWave),
-                     0, s, A, offsets, E, rows, B0, B1, N, K, out, ntn);
+  hipLaunchKernelGGL((grouped_gemm_bf16<BM, BN, BK, WM, WN, GATEUP, MAXW>), grid,
+                     dim3(WM * WN * kWave), 0, s, A, offsets, E, rows, B0, B1, N, K, out, ntn,
+                     (int)n_tiles);
+}
+
+template <int BM, int BN, int WM, int WN, bool GATEUP, int NSETS, int MAXW>
+void launch_gemm_pipe(const bf16* A, const int32_t* offsets, int E, int rows, const bf16* B0,
+                      const bf16* B1, int N, int K, bf16* out, hipStream_t s, const char* name) {
+  const int ntn = ceil_div(N, BN);
+  const int max_mt = ceil_div(rows, BM) + E;
+  const long long n_tiles = (long long)max_mt * ntn;
+  dim3 grid((unsigned)((n_tiles + 7) / 8 * 8));
+  ProfileScope ps(name, s);
+  hipLaunchKernelGGL((grouped_gemm_bf16_pipe<BM, BN, WM, WN, GATEUP, NSETS, MAXW>), grid,
+                     dim3(WM * WN * kWave), 0, s, A, offsets, E, rows, B0, B1, N, K, out, ntn,
+                     (int)n_tiles);
 }
 
 }  // namespace
@@ -313,11 +748,36 @@ hipError_t launch_expert_ffn(foe_dtype dt, int E, int d, int F, int rows, const 
   bf16* y = reinterpret_cast<bf16*>(y_perm);
   const bool small_m = rows < 64 * E;  // few rows per expert: weight-streaming bound
   if (small_m) {
-    launch_gemm<32, 64, 64, 1, 2, true>(xp, offsets, E, rows, wg, wu, F, d, h, s, "ffn_gateup");
-    launch_gemm<32, 64, 64, 1, 2, false>(h, offsets, E, rows, wd, nullptr, d, F, y, s, "ffn_down");
+#ifdef FOE_OLD_DECODE
+    launch_gemm<FOE_DEC_GU, true, 4>(xp, offsets, E, rows, wg, wu, F, d, h, s, "ffn_gateup");
+    launch_gemm<FOE_DEC_DN, false, 4>(h, offsets, E, rows, wd, nullptr, d, F, y, s, "ffn_down");
+#else
+    {
+      const int ng = ceil_div(F, 16);
+      ProfileScope ps("ffn_gateup", s);
+      hipLaunchKernelGGL((ffn_skinny_bf16<true, FOE_SKINNY>), dim3(E * ng),
+                         dim3(kSkinnyWaves * kWave), 0, s, xp, offsets, E, rows, wg, wu, F, d, h, ng);
+    }
+    {
+      const int ng = ceil_div(d, 32);
+      ProfileScope ps("ffn_down", s);
+      hipLaunchKernelGGL((ffn_skinny_bf16<false, FOE_SKINNY>), dim3(E * ng),
+                         dim3(kSkinnyWaves * kWave), 0, s, h, offsets, E, rows, wd, nullptr, d, F, y,
+                         ng);
+    }
+#endif
   } else {
-    launch_gemm<128, 128, 32, 2, 2, true>(xp, offsets, E, rows, wg, wu, F, d, h, s, "ffn_gateup");
-    launch_gemm<128, 128, 32, 2, 2, false>(h, offsets, E, rows, wd, nullptr, d, F, y, s, "ffn_down");
+#ifdef FOE_OLD_PREFILL
+    launch_gemm<FOE_PRE_GU, true, FOE_PRE_OCC>(xp, offsets, E, rows, wg, wu, F, d, h, s,
+                                              "ffn_gateup");
+    launch_gemm<FOE_PRE_DN, false, FOE_PRE_OCC>(h, offsets, E, rows, wd, nullptr, d, F, y, s,
+                                               "ffn_down");
+#else
+    launch_gemm_pipe<FOE_PIPE_GU, true, FOE_PIPE_OPT>(xp, offsets, E, rows, wg, wu, F, d, h, s,
+                                                   "ffn_gateup");
+    launch_gemm_pipe<FOE_PIPE_DN, false, FOE_PIPE_OPT>(h, offsets, E, rows, wd, nullptr, d, F, y, s,
+                                                    "ffn_down");
+#endif
   }
   return hipGetLastError();
 }

@@ -126,6 +126,85 @@ __global__ __launch_bounds__(256) void rank_kernel(const int32_t* __restrict__ i
   }
 }
 
+// Small R: histogram, scan and stable ranks in one workgroup of 16 waves.
+// Wave w owns the contiguous pairs [w*per, (w+1)*per); per-wave counts give
+// every wave its base per expert, then each wave ranks its pairs in flat
+// order with the same ballot walk as rank_kernel.
+constexpr int kSmallWaves = 16;
+constexpr int kSmallMaxR = 8192;
+
+__global__ __launch_bounds__(kSmallWaves * 64) void index_small_kernel(
+    const int32_t* __restrict__ idx, int R, int E, int32_t* __restrict__ counts,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_src,
+    int32_t* __restrict__ row_of) {
+  __shared__ int wcnt[kSmallWaves][kMaxE];
+  __shared__ int total[kMaxE + 1];
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  for (int i = threadIdx.x; i < kSmallWaves * kMaxE; i += blockDim.x) (&wcnt[0][0])[i] = 0;
+  __syncthreads();
+  const int per = (R + kSmallWaves * kWave - 1) / (kSmallWaves * kWave) * kWave;
+  const int start = wave * per;
+  const int end = min(start + per, R);
+  for (int f = start + lane; f < end; f += kWave) {
+    const int e = idx[f];
+    if (e >= 0 && e < E) atomicAdd(&wcnt[wave][e], 1);
+  }
+  __syncthreads();
+  if (threadIdx.x < E) {
+    const int e = threadIdx.x;
+    int run = 0;
+    for (int w = 0; w < kSmallWaves; ++w) run += wcnt[w][e];
+    total[e] = run;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int i = 0; i < E; ++i) {
+      const int c = total[i];
+      total[i] = run;
+      run += c;
+    }
+    total[E] = run;
+  }
+  __syncthreads();
+  if (threadIdx.x < E) {
+    const int e = threadIdx.x;
+    int run = total[e];
+    offsets[e] = run;
+    if (counts != nullptr) counts[e] = total[e + 1] - run;
+    for (int w = 0; w < kSmallWaves; ++w) {
+      const int c = wcnt[w][e];
+      wcnt[w][e] = run;
+      run += c;
+    }
+  }
+  if (threadIdx.x == 0) offsets[E] = total[E];
+  __syncthreads();
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int f0 = start; f0 < end; f0 += kWave) {
+    const int f = f0 + lane;
+    const bool valid = f < end;
+    const int e = valid ? idx[f] : -1;
+    const bool ok = valid && e >= 0 && e < E;
+    if (valid && !ok) row_of[f] = -1;
+    uint64_t remaining = __ballot(ok);
+    while (remaining) {
+      const int leader = __builtin_ctzll(remaining);
+      const int v = __builtin_amdgcn_readlane(e, leader);
+      const uint64_t m = __ballot(ok && e == v);
+      const int base = wcnt[wave][v];
+      if (ok && e == v) {
+        const int p = base + __popcll(m & lt_mask);
+        sorted_src[p] = f;
+        row_of[f] = p;
+      }
+      if (lane == leader) wcnt[wave][v] = base + __popcll(m);
+      remaining &= ~m;
+    }
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void scatter_rows_kernel(const T* __restrict__ x,
                                                            const int32_t* __restrict__ row_of,
@@ -190,6 +269,11 @@ hipError_t launch_permute(foe_dtype dt, int T, int d, int E, int k, const int32_
   const int nblk = permute_blocks(R);
   int32_t* block_counts = reinterpret_cast<int32_t*>(scratch);
   int32_t* block_base = block_counts + (size_t)nblk * E;
+  if (R <= kSmallMaxR) {
+    ProfileScope ps("permute_index", s);
+    hipLaunchKernelGGL(index_small_kernel, dim3(1), dim3(kSmallWaves * kWave), 0, s, topk_idx, R,
+                       E, counts, offsets, sorted_src, row_of);
+  } else {
   {
     ProfileScope ps("permute_hist", s);
     hipLaunchKernelGGL(hist_kernel, dim3(nblk), dim3(256), 0, s, topk_idx, R, E, block_counts);
@@ -203,6 +287,7 @@ hipError_t launch_permute(foe_dtype dt, int T, int d, int E, int k, const int32_
     ProfileScope ps("permute_rank", s);
     hipLaunchKernelGGL(rank_kernel, dim3(nblk), dim3(256), 0, s, topk_idx, R, E, block_base,
                        sorted_src, row_of);
+  }
   }
   {
     ProfileScope ps("permute_scatter", s);

@@ -1,19 +1,20 @@
 // Router scores + per-group top-k + softmax weights (Section 3.1, routing
 // equation), fused in one kernel: the [T,E] scores never leave the chip.
 //
-// One workgroup = 4 waves = 16 tokens.  The score tile S[16 tokens][E] is a
-// skinny GEMM x[16,d] * W_r[E,d]^T on MFMA (bf16: 16x16x32, fp32: 16x16x4)
-// with K split across the 4 waves; the 4 partial tiles are summed in LDS in a
-// fixed order.  In the 16x16 MFMA result layout each row of 16 lanes holds all
-// 16 experts of one token (per accumulator register), so the top-k is k rounds
-// of a (score desc, id asc) arg-max across a 16-lane row with DPP rotations.
+// One workgroup = 16 tokens, 4 or 8 waves.  The score tile S[16 tokens][E] is
+// a skinny GEMM x[16,d] * W_r[E,d]^T on MFMA (bf16: 16x16x32, fp32: 16x16x4)
+// with K split across the waves (each issuing the loads of several K steps at
+// once); the partial tiles are summed in LDS in a fixed order.  In the 16x16
+// MFMA result layout each row of 16 lanes holds all 16 experts of one token
+// (per accumulator register), so the top-k is k rounds of a (score desc, id
+// asc) arg-max across a 16-lane row with DPP rotations.
 #include "foe_common.hpp"
 
 namespace foe {
 namespace {
 
 constexpr int kTok = 16;    // tokens per workgroup
-constexpr int kWaves = 4;   // K split
+constexpr int kBatch = 4;   // K steps whose loads are issued together
 
 // (v, e) beats (w, f): larger score, equal scores -> lower id
 __device__ __forceinline__ bool beats(float v, int e, float w, int f) {
@@ -33,7 +34,7 @@ template <typename T> struct RouteMma;
 // x[r][kc + 8q .. +8) and W_r[e][same k] — the same k map on both operands.
 template <> struct RouteMma<bf16> {
   static constexpr int KSTEP = 32;
-  template <int NT>
+  template <int NT, int NW>
   __device__ static void run(const bf16* x, const bf16* w, int T, int d, int E, int t0,
                              int wave, int lane, f32x4 (&acc)[NT]) {
     const int r = lane & 15, q = lane >> 4;
@@ -41,21 +42,28 @@ template <> struct RouteMma<bf16> {
     const bool tok_ok = tok < T;
     const bf16* xrow = x + (size_t)(tok_ok ? tok : 0) * d;
     const int nsteps = (d + KSTEP - 1) / KSTEP;
-    for (int c = wave; c < nsteps; c += kWaves) {
-      const int kb = c * KSTEP + q * 8;
-      const bool k_ok = kb < d;
-      u32x4 a = (tok_ok && k_ok) ? *reinterpret_cast<const u32x4*>(xrow + kb) : zero_u32x4();
-      u32x4 b[NT];
+    // wave w takes K-step groups w, w+NW, ... of kBatch steps each
+    for (int c0 = wave * kBatch; c0 < nsteps; c0 += NW * kBatch) {
+      u32x4 a[kBatch], b[kBatch][NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int e = nt * 16 + r;
-        b[nt] = (e < E && k_ok) ? *reinterpret_cast<const u32x4*>(w + (size_t)e * d + kb)
-                                : zero_u32x4();
+      for (int u = 0; u < kBatch; ++u) {
+        const int kb = (c0 + u) * KSTEP + q * 8;
+        const bool k_ok = c0 + u < nsteps && kb < d;
+        a[u] = (tok_ok && k_ok) ? *reinterpret_cast<const u32x4*>(xrow + kb) : zero_u32x4();
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int e = nt * 16 + r;
+          b[u][nt] = (e < E && k_ok) ? *reinterpret_cast<const u32x4*>(w + (size_t)e * d + kb)
+                                     : zero_u32x4();
+        }
       }
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            __builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b[nt]), acc[nt], 0, 0, 0);
+      for (int u = 0; u < kBatch; ++u)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+          acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[u]),
+                                                            __builtin_bit_cast(bf16x8, b[u][nt]),
+                                                            acc[nt], 0, 0, 0);
     }
   }
 };
@@ -64,7 +72,7 @@ template <> struct RouteMma<bf16> {
 // s-th using element s (k map kc + 4q + s on both operands).
 template <> struct RouteMma<float> {
   static constexpr int KSTEP = 16;
-  template <int NT>
+  template <int NT, int NW>
   __device__ static void run(const float* x, const float* w, int T, int d, int E, int t0,
                              int wave, int lane, f32x4 (&acc)[NT]) {
     const int r = lane & 15, q = lane >> 4;
@@ -72,7 +80,7 @@ template <> struct RouteMma<float> {
     const bool tok_ok = tok < T;
     const float* xrow = x + (size_t)(tok_ok ? tok : 0) * d;
     const int nsteps = (d + KSTEP - 1) / KSTEP;
-    for (int c = wave; c < nsteps; c += kWaves) {
+    for (int c = wave; c < nsteps; c += NW) {
       const int kb = c * KSTEP + q * 4;
       const bool k_ok = kb < d;
       f32x4 a = (tok_ok && k_ok) ? *reinterpret_cast<const f32x4*>(xrow + kb)
@@ -91,8 +99,8 @@ template <> struct RouteMma<float> {
   }
 };
 
-template <typename T, int NT>
-__global__ __launch_bounds__(256) void route_kernel(const T* __restrict__ x,
+template <typename T, int NT, int NW>
+__global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
                                                     const T* __restrict__ w,
                                                     const float* __restrict__ bias, int T_,
                                                     int d, int E, int k,
@@ -106,29 +114,33 @@ __global__ __launch_bounds__(256) void route_kernel(const T* __restrict__ x,
   f32x4 acc[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  RouteMma<T>::template run<NT>(x, w, T_, d, E, t0, wave, lane, acc);
+  RouteMma<T>::template run<NT, NW>(x, w, T_, d, E, t0, wave, lane, acc);
 
-  // partial tiles of the 4 waves -> LDS [wave][nt][lane] (f32x4)
+  // partial tiles of the NW waves -> LDS [wave][nt][lane] (f32x4)
   f32x4* part = reinterpret_cast<f32x4*>(smem);
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) part[(wave * NT + nt) * kWave + lane] = acc[nt];
   __syncthreads();
 
-  // wave `wave` owns accumulator register i = wave: token 4*(lane/16) + wave,
-  // expert nt*16 + lane%16.  Sum the 4 partials in wave order.
+  // wave `wave` (< 4) owns accumulator register i = wave: token
+  // 4*(lane/16) + wave, expert nt*16 + lane%16.  Sum the NW partials in wave
+  // order.
   const int col = lane & 15;
-  const int tl = 4 * (lane >> 4) + wave;  // token within the workgroup
+  const int tl = 4 * (lane >> 4) + (wave & 3);  // token within the workgroup
   float g[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     float s = 0.f;
+    if (wave < 4) {
 #pragma unroll
-    for (int w4 = 0; w4 < kWaves; ++w4) s += part[(w4 * NT + nt) * kWave + lane][wave];
-    const int e = nt * 16 + col;
-    if (bias != nullptr && e < E) s += bias[e];
+      for (int w = 0; w < NW; ++w) s += part[(w * NT + nt) * kWave + lane][wave];
+      const int e = nt * 16 + col;
+      if (bias != nullptr && e < E) s += bias[e];
+    }
     g[nt] = s;
   }
   __syncthreads();  // partial tiles are dead; LDS is reused for the selection
+  if (wave >= 4) return;  // no barrier follows
 
   int* sel_e = reinterpret_cast<int*>(smem);
   float* sel_v = reinterpret_cast<float*>(smem) + kTok * k;
@@ -156,7 +168,8 @@ __global__ __launch_bounds__(256) void route_kernel(const T* __restrict__ x,
       sel_v[tl * k + s] = bv;
     }
   }
-  __syncthreads();
+  // each wave reads back only its own tokens' selections (LDS operations of
+  // one wave complete in order)
 
   // softmax over the selected scores; lane col writes slots col, col+16, ...
   const int tok = t0 + tl;
@@ -172,28 +185,30 @@ __global__ __launch_bounds__(256) void route_kernel(const T* __restrict__ x,
   }
 }
 
-template <typename T, int NT>
+template <typename T, int NT, int NW>
 hipError_t launch_nt(int T_, int d, int E, int k, const void* x, const void* w,
                      const float* bias, int32_t* idx, float* wt, hipStream_t s) {
-  size_t lds_red = (size_t)kWaves * NT * kWave * sizeof(f32x4);
+  size_t lds_red = (size_t)NW * NT * kWave * sizeof(f32x4);
   size_t lds_sel = (size_t)kTok * k * 8;
   size_t lds = lds_red > lds_sel ? lds_red : lds_sel;
   dim3 grid(ceil_div(T_, kTok));
   ProfileScope ps("route", s);
-  hipLaunchKernelGGL((route_kernel<T, NT>), grid, dim3(256), lds, s,
+  hipLaunchKernelGGL((route_kernel<T, NT, NW>), grid, dim3(NW * kWave), lds, s,
                      reinterpret_cast<const T*>(x), reinterpret_cast<const T*>(w), bias, T_, d,
                      E, k, idx, wt);
   return hipGetLastError();
 }
 
+// 8 waves split K when the partial tiles are small (more loads in flight per
+// token group), 4 when E is large
 template <typename T>
 hipError_t launch_t(int T_, int d, int E, int k, const void* x, const void* w, const float* bias,
                     int32_t* idx, float* wt, hipStream_t s) {
-  if (E <= 16) return launch_nt<T, 1>(T_, d, E, k, x, w, bias, idx, wt, s);
-  if (E <= 32) return launch_nt<T, 2>(T_, d, E, k, x, w, bias, idx, wt, s);
-  if (E <= 64) return launch_nt<T, 4>(T_, d, E, k, x, w, bias, idx, wt, s);
-  if (E <= 128) return launch_nt<T, 8>(T_, d, E, k, x, w, bias, idx, wt, s);
-  return launch_nt<T, 16>(T_, d, E, k, x, w, bias, idx, wt, s);
+  if (E <= 16) return launch_nt<T, 1, 8>(T_, d, E, k, x, w, bias, idx, wt, s);
+  if (E <= 32) return launch_nt<T, 2, 8>(T_, d, E, k, x, w, bias, idx, wt, s);
+  if (E <= 64) return launch_nt<T, 4, 8>(T_, d, E, k, x, w, bias, idx, wt, s);
+  if (E <= 128) return launch_nt<T, 8, 4>(T_, d, E, k, x, w, bias, idx, wt, s);
+  return launch_nt<T, 16, 4>(T_, d, E, k, x, w, bias, idx, wt, s);
 }
 
 }  // namespace
