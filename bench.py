@@ -52,23 +52,23 @@ def parse():
 
 
 def kernel_work(name, cfg, e_touched):
-    """Algorithmic (flops, bytes) of ONE launch of kernel `name` (one cluster)."""
+    """Algorithmic (flops, bytes) of ONE launch of kernel `name` in a
+    foe_cluster_block step.  Route runs once per cluster; the index pass, the
+    two grouped FFN kernels (all C*E experts) and the combine + reduction run
+    once per step.  `e_touched` = experts (over all clusters) that got rows."""
     T, d, E, k, F, C = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["F"], cfg["C"]
     s = 2 if cfg["dtype"] == "bf16" else 4
-    R = T * k
+    R = T * k          # pairs per cluster
+    CR = C * R         # permuted rows over all clusters
     if name == "route":
         return 2.0 * T * d * E, T * d * s + E * d * s + 8.0 * R
-    if name == "permute_scatter":
-        return 0.0, T * d * s + R * d * s + 4.0 * R
     if name in ("ffn_gateup", "ffn_gateup_f32"):
-        return 4.0 * R * d * F, 2.0 * e_touched * F * d * s + R * d * s + R * F * s
+        return 4.0 * CR * d * F, 2.0 * e_touched * F * d * s + CR * d * s + CR * F * s
     if name in ("ffn_down", "ffn_down_f32"):
-        return 2.0 * R * F * d, 1.0 * e_touched * d * F * s + R * F * s + R * d * s
+        return 2.0 * CR * F * d, 1.0 * e_touched * d * F * s + CR * F * s + CR * d * s
     if name == "combine":
-        direct = C == 1
-        return 2.0 * R * d, R * d * s + 8.0 * R + (2 if direct else 1) * T * d * s
-    if name == "reduce":
-        return 2.0 * C * T * d, (C + 2.0) * T * d * s
+        # y rows of every cluster, their indices and weights, x, out
+        return 2.0 * CR * d, CR * d * s + 8.0 * CR + 2.0 * T * d * s
     return 0.0, 0.0
 
 
@@ -181,14 +181,14 @@ def main():
         if rc != 0:
             raise RuntimeError(foe.last_error())
 
-    # experts that received rows (for the weight-streaming bytes); outside timing
-    e_touched = []
+    # experts (over all clusters) that received rows, for the weight-streaming
+    # bytes; computed outside the timed region
+    e_touched = 0
     for h in range(C):
         st = sets[0]
         idx, _ = foe.route(st["x"], st["w_router"][h], None if st["bias"] is None else st["bias"][h], k)
         p = foe.permute(idx, st["x"], E)
-        e_touched.append(int((p["counts"] > 0).sum().item()))
-    e_touched = sum(e_touched) / C
+        e_touched += int((p["counts"] > 0).sum().item())
 
     def timed(n_steps, run):
         torch.cuda.synchronize()

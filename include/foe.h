@@ -122,6 +122,7 @@ int foe_permute(foe_dtype dt, int T, int d, int E, int k,
  *   w_down          [E,d,F]   dt
  *   y_perm          [rows,d]  dt out (rows outside every segment are not written)
  *   ws, ws_bytes    workspace of foe_workspace_bytes("expert_ffn", ...)
+ * bf16 limits: rows*d and rows*F below 2^30 elements (else FOE_ERR_UNSUPPORTED).
  */
 int foe_expert_ffn(foe_dtype dt, int E, int d, int F, int rows,
                    const void* x_perm, const int32_t* expert_offsets,
@@ -164,8 +165,12 @@ int foe_reduce(foe_dtype dt, int C, int T, int d,
  * update" rows), followed by the local reduction:
  *   out = reduce_scale * sum_h (x + delta_h),
  *   delta_h[i] = sum_{e in I_h[i]} w_h[i,e] FFN_{h,e}(x[i]).
- * Each cluster runs route -> permute -> expert FFN -> combine; the per-cluster
- * partials live in the workspace.
+ * Routing runs per cluster; the dispatch of all clusters is numbered in one
+ * pass, one grouped FFN covers all C*E experts and reads the rows of x through
+ * the permutation (no permuted copy of x is written), and one kernel forms
+ * every cluster's weighted sum and the reduction (no per-cluster partial is
+ * written).  Evaluated as reduce_scale * (C * x + S) with S the fp32 sum of
+ * the weighted expert rows in the order (h = 0..C-1, j = 0..k-1).
  *
  *   x         [T,d]       dt
  *   w_router  [C,E,d]     dt;   bias [C,E] fp32 or NULL
@@ -173,6 +178,8 @@ int foe_reduce(foe_dtype dt, int C, int T, int d,
  *   reduce_scale          1/C = the paper's average, 1 = a plain sum
  *   out       [T,d]       dt out
  *   ws, ws_bytes          workspace of foe_workspace_bytes("cluster_block", ...)
+ * bf16 limits: T*d, C*T*k*d and C*T*k*F below 2^30 elements (else
+ * FOE_ERR_UNSUPPORTED); C*T*k below 2^31.
  */
 int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F,
                       const void* x, const void* w_router, const float* bias,

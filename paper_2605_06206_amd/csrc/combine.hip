@@ -78,6 +78,72 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
   }
 }
 
+// Fused combine + local reduction of C co-resident clusters that share the
+// input x:  out[i] = scale * sum_h (x[i] + sum_j w_h[i,j] * y[row_of_h[i*k+j]])
+// with y holding the FFN rows of every cluster (row_of values index it
+// directly).  Evaluated as scale * (C * x[i] + S) where S sums the weighted
+// rows in the order (h = 0..C-1, j = 0..k-1) in fp32; the per-cluster partials
+// never reach HBM.
+template <typename T>
+__global__ __launch_bounds__(256) void combine_clusters_kernel(
+    const T* __restrict__ y, const int32_t* __restrict__ row_of_all,
+    const float* __restrict__ w_all, const T* __restrict__ x, int C, int T_, int d, int k,
+    int y_rows, float scale, T* __restrict__ out) {
+  constexpr int EPV = Vec16<T>::N;
+  constexpr int U = 4;
+  const int lane = lane_id();
+  const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (tok >= T_) return;
+  const size_t R = (size_t)T_ * k;
+  const int nvec = d / EPV;
+  const float cx = (float)C;
+  for (int c0 = 0; c0 < nvec; c0 += U * kWave) {
+    float acc[U][EPV];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) acc[u][e] = 0.f;
+    for (int h = 0; h < C; ++h) {
+      const int32_t* rows = row_of_all + h * R + (size_t)tok * k;
+      const float* wts = w_all + h * R + (size_t)tok * k;
+      for (int j = 0; j < k; j += 2) {
+        const bool two = j + 1 < k;
+        const int p0 = rows[j], p1 = two ? rows[j + 1] : -1;
+        const float w0 = wts[j], w1 = two ? wts[j + 1] : 0.f;
+        const bool ok0 = p0 >= 0 && p0 < y_rows, ok1 = p1 >= 0 && p1 < y_rows;
+        Vec16<T> v0[U], v1[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int c = c0 + u * kWave + lane;
+          if (c < nvec && ok0) v0[u] = load16(y + (size_t)p0 * d + (size_t)c * EPV);
+          if (c < nvec && ok1) v1[u] = load16(y + (size_t)p1 * d + (size_t)c * EPV);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (ok0) {
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) acc[u][e] = fmaf(w0, to_f32(v0[u].v[e]), acc[u][e]);
+          }
+          if (ok1) {
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) acc[u][e] = fmaf(w1, to_f32(v1[u].v[e]), acc[u][e]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + u * kWave + lane;
+      if (c >= nvec) continue;
+      const Vec16<T> xv = load16(x + (size_t)tok * d + (size_t)c * EPV);
+      Vec16<T> o;
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) o.v[e] = from_f32<T>(scale * fmaf(cx, to_f32(xv.v[e]), acc[u][e]));
+      store16(out + (size_t)tok * d + (size_t)c * EPV, o);
+    }
+  }
+}
+
 // out = scale * sum_h (res + P_h), h = 0..C-1 in order; one 16-byte vector per
 // thread per grid-stride step.
 template <typename T>
@@ -127,6 +193,26 @@ hipError_t launch_combine(foe_dtype dt, int T, int d, int k, const void* y_perm,
     hipLaunchKernelGGL(combine_kernel<float>, grid, dim3(256), 0, s,
                        reinterpret_cast<const float*>(y_perm), row_of, topk_w,
                        reinterpret_cast<const float*>(residual), T, d, k,
+                       reinterpret_cast<float*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_clusters(foe_dtype dt, int C, int T, int d, int k, const void* y,
+                                   const int32_t* row_of_all, const float* w_all, const void* x,
+                                   float scale, void* out, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const int y_rows = C * T * k;
+  dim3 grid(ceil_div(T, 4));
+  ProfileScope ps("combine", s);
+  if (dt == FOE_BF16)
+    hipLaunchKernelGGL(combine_clusters_kernel<bf16>, grid, dim3(256), 0, s,
+                       reinterpret_cast<const bf16*>(y), row_of_all, w_all,
+                       reinterpret_cast<const bf16*>(x), C, T, d, k, y_rows, scale,
+                       reinterpret_cast<bf16*>(out));
+  else
+    hipLaunchKernelGGL(combine_clusters_kernel<float>, grid, dim3(256), 0, s,
+                       reinterpret_cast<const float*>(y), row_of_all, w_all,
+                       reinterpret_cast<const float*>(x), C, T, d, k, y_rows, scale,
                        reinterpret_cast<float*>(out));
   return hipGetLastError();
 }

@@ -62,31 +62,41 @@ void check_route_shape(Check& c, int T, int E, int k) {
   c.need((long long)T * (k < 1 ? 1 : k) <= INT_MAX, "T*k must fit in int32");
 }
 
+// 16-byte operand loads address their buffers with 32-bit byte offsets below
+// 2^31 (larger offsets mean "read zeros"), which bounds the bf16 tensors that
+// are read that way.
+constexpr long long kMaxOperandBytes = (1ll << 31) - 64;
+bool operand_fits(long long rows, long long cols, size_t el) {
+  return rows * cols * (long long)el <= kMaxOperandBytes;
+}
+
 // ---- workspace layout of foe_cluster_block ---------------------------------
+// All C clusters are processed together: routing of cluster h fills slice h of
+// topk_idx / topk_w [C,T,k]; one index pass numbers the permuted rows of all
+// clusters consecutively (cluster h from h*T*k); one grouped FFN runs over the
+// C*E experts reading x through sorted_src; one kernel combines and reduces.
 struct BlockWs {
-  size_t topk_idx, topk_w, counts, offsets, sorted_src, row_of, x_perm, y, perm, ffn, deltas, total;
+  size_t topk_idx, topk_w, counts, offsets, sorted_src, row_of, y, perm, ffn, total;
 };
 
 BlockWs block_ws(foe_dtype dt, int C, int T, int d, int E, int k, int F) {
   BlockWs w{};
-  const size_t R = (size_t)T * k, s = esize(dt);
+  const size_t R = (size_t)T * k, CR = (size_t)C * R, CE = (size_t)C * E, s = esize(dt);
   size_t off = 0;
   auto take = [&](size_t& field, size_t bytes) {
     off = align_up(off, 256);
     field = off;
     off += bytes;
   };
-  take(w.topk_idx, R * 4);
-  take(w.topk_w, R * 4);
-  take(w.counts, (size_t)E * 4);
-  take(w.offsets, (size_t)(E + 1) * 4);
-  take(w.sorted_src, R * 4);
-  take(w.row_of, R * 4);
-  take(w.x_perm, R * d * s);
-  take(w.y, R * d * s);
+  take(w.topk_idx, CR * 4);
+  take(w.topk_w, CR * 4);
+  take(w.counts, CE * 4);
+  take(w.offsets, (CE + 1) * 4);
+  take(w.sorted_src, CR * 4);
+  take(w.row_of, CR * 4);
+  take(w.y, CR * d * s);
   take(w.perm, permute_scratch_bytes(T, k, E));
-  take(w.ffn, ffn_scratch_bytes(dt, (int)R, F));
-  take(w.deltas, (size_t)C * T * d * s);
+  take(w.ffn, ffn_scratch_bytes(dt, (int)CR, F));
   w.total = align_up(off, 256);
   return w;
 }
@@ -164,6 +174,7 @@ size_t foe_workspace_bytes(const char* op, foe_dtype dt, int C, int T, int d, in
   if (o == "cluster_block") {
     check_route_shape(c, T, E, k);
     c.need(C >= 1 && C <= 64, "C must be in [1, 64]");
+    c.need((long long)C * T * (k < 1 ? 1 : k) <= INT_MAX, "C*T*k must fit in int32");
     check_dim8(c, d, "d must be a positive multiple of 8");
     check_dim8(c, F, "F must be a positive multiple of 8");
     if (!c.err.empty()) return (g_err = c.err, SIZE_MAX);
@@ -238,6 +249,8 @@ int foe_expert_ffn(foe_dtype dt, int E, int d, int F, int rows, const void* x_pe
   c.tensor(w_down, any, "w_down");
   c.tensor(y_perm, any, "y_perm");
   if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_expert_ffn: " + c.err);
+  if (dt == FOE_BF16 && !(operand_fits(rows, d, 2) && operand_fits(rows, F, 2)))
+    return fail(FOE_ERR_UNSUPPORTED, "foe_expert_ffn: rows*d and rows*F must stay below 2^30 bf16 elements");
   const size_t need = any ? ffn_scratch_bytes(dt, rows, F) : 0;
   if (need > 0 && (ws == nullptr || !aligned16(ws)))
     return fail(FOE_ERR_INVALID, "foe_expert_ffn: ws is NULL or not 16-byte aligned");
@@ -297,6 +310,7 @@ int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F, co
   check_dtype(c, dt);
   c.need(C >= 1 && C <= 64, "C must be in [1, 64]");
   check_route_shape(c, T, E, k);
+  c.need((long long)C * T * (k < 1 ? 1 : k) <= INT_MAX, "C*T*k must fit in int32");
   check_dim8(c, d, "d must be a positive multiple of 8");
   check_dim8(c, F, "F must be a positive multiple of 8");
   const bool any = T > 0;
@@ -309,6 +323,10 @@ int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F, co
   c.tensor(out, any, "out");
   if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_cluster_block: " + c.err);
   if (!any) return FOE_OK;
+  const long long CR = (long long)C * T * k;
+  if (dt == FOE_BF16 && !(operand_fits(T, d, 2) && operand_fits(CR, F, 2) && operand_fits(CR, d, 2)))
+    return fail(FOE_ERR_UNSUPPORTED,
+                "foe_cluster_block: T*d, C*T*k*F and C*T*k*d must stay below 2^30 bf16 elements");
   const BlockWs L = block_ws(dt, C, T, d, E, k, F);
   if (ws == nullptr || !aligned16(ws))
     return fail(FOE_ERR_INVALID, "foe_cluster_block: ws is NULL or not 16-byte aligned");
@@ -325,42 +343,32 @@ int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F, co
   int32_t* offsets = reinterpret_cast<int32_t*>(base + L.offsets);
   int32_t* sorted_src = reinterpret_cast<int32_t*>(base + L.sorted_src);
   int32_t* row_of = reinterpret_cast<int32_t*>(base + L.row_of);
-  void* x_perm = base + L.x_perm;
   void* y = base + L.y;
   void* perm_ws = base + L.perm;
   void* ffn_ws = base + L.ffn;
-  unsigned char* deltas = base + L.deltas;
 
   const size_t s_el = esize(dt);
-  const int R = T * k;
-  const bool direct = (C == 1 && reduce_scale == 1.0f);  // out = x + delta in one pass
+  const size_t R = (size_t)T * k;
   const unsigned char* wr = reinterpret_cast<const unsigned char*>(w_router);
-  const unsigned char* wg = reinterpret_cast<const unsigned char*>(w_gate);
-  const unsigned char* wu = reinterpret_cast<const unsigned char*>(w_up);
-  const unsigned char* wd = reinterpret_cast<const unsigned char*>(w_down);
+  // 1. routing of every cluster (Section 3.1: one score vector, per-group top-k)
   for (int h = 0; h < C; ++h) {
-    const size_t wr_off = (size_t)h * E * d * s_el;
-    const size_t wx_off = (size_t)h * E * F * d * s_el;
-    hipError_t e = launch_route(dt, T, d, E, k, x, wr + wr_off,
-                                bias ? bias + (size_t)h * E : nullptr, topk_idx, topk_w, s);
+    hipError_t e = launch_route(dt, T, d, E, k, x, wr + (size_t)h * E * d * s_el,
+                                bias ? bias + (size_t)h * E : nullptr, topk_idx + h * R,
+                                topk_w + h * R, s);
     if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/route");
-    e = launch_permute(dt, T, d, E, k, topk_idx, x, counts, offsets, sorted_src, row_of, x_perm,
-                       perm_ws, s);
-    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/permute");
-    e = launch_expert_ffn(dt, E, d, F, R, x_perm, offsets, wg + wx_off, wu + wx_off,
-                          wd + wx_off, y, ffn_ws, s);
-    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/expert_ffn");
-    if (direct)
-      e = launch_combine(dt, T, d, k, y, row_of, topk_w, x, out, s);
-    else
-      e = launch_combine(dt, T, d, k, y, row_of, topk_w, nullptr,
-                         deltas + (size_t)h * T * d * s_el, s);
-    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/combine");
   }
-  if (!direct) {
-    hipError_t e = launch_reduce(dt, C, T, d, deltas, x, reduce_scale, out, s);
-    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/reduce");
-  }
+  // 2. dispatch: expert histogram, prefix sum and stable ranks of all clusters
+  hipError_t e =
+      launch_index(T, E, k, C, topk_idx, counts, offsets, sorted_src, row_of, perm_ws, s);
+  if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/index");
+  // 3. one grouped SwiGLU FFN over the C*E experts (weights are [C*E, ...]),
+  //    reading the rows of x through sorted_src
+  e = launch_expert_ffn_ex(dt, C * E, d, F, (int)CR, x, sorted_src, k, T, offsets, w_gate, w_up,
+                           w_down, y, ffn_ws, s);
+  if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/expert_ffn");
+  // 4. weighted combine of every cluster and the local cross-cluster reduction
+  e = launch_combine_clusters(dt, C, T, d, k, y, row_of, topk_w, x, reduce_scale, out, s);
+  if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/combine");
   return FOE_OK;
 }
 

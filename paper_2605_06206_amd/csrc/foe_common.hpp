@@ -83,6 +83,11 @@ hipError_t launch_route(foe_dtype dt, int T, int d, int E, int k, const void* x,
 // permute scratch = 2 * nblk * E int32 (see permute_blocks())
 int permute_blocks(int R);
 size_t permute_scratch_bytes(int T, int k, int E);
+// histogram / scan / stable ranks of C clusters' ids (topk_idx [C,T,k]);
+// offsets [C*E+1] and row_of values are global rows (cluster h starts at h*T*k)
+hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int32_t* counts,
+                        int32_t* offsets, int32_t* sorted_src, int32_t* row_of, void* scratch,
+                        hipStream_t s);
 hipError_t launch_permute(foe_dtype dt, int T, int d, int E, int k, const int32_t* topk_idx,
                           const void* x, int32_t* counts, int32_t* offsets, int32_t* sorted_src,
                           int32_t* row_of, void* x_perm, void* scratch, hipStream_t s);
@@ -92,6 +97,15 @@ hipError_t launch_expert_ffn(foe_dtype dt, int E, int d, int F, int rows, const 
                              const int32_t* offsets, const void* w_gate, const void* w_up,
                              const void* w_down, void* y_perm, void* scratch, hipStream_t s);
 
+// expert FFN whose operand row r is row gather[r]/kdiv of A (a_rows rows);
+// gather == nullptr: row r of A
+hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, const void* A,
+                                const int32_t* gather, int kdiv, int a_rows,
+                                const int32_t* offsets, const void* w_gate, const void* w_up,
+                                const void* w_down, void* y_perm, void* scratch, hipStream_t s);
+hipError_t launch_combine_clusters(foe_dtype dt, int C, int T, int d, int k, const void* y,
+                                   const int32_t* row_of_all, const float* w_all, const void* x,
+                                   float scale, void* out, hipStream_t s);
 hipError_t launch_combine(foe_dtype dt, int T, int d, int k, const void* y_perm,
                           const int32_t* row_of, const float* topk_w, const void* residual,
                           void* out, hipStream_t s);

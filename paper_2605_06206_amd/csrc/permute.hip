@@ -41,7 +41,8 @@ __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ b
                                                    int nblk, int E,
                                                    int32_t* __restrict__ counts,
                                                    int32_t* __restrict__ offsets,
-                                                   int32_t* __restrict__ block_base) {
+                                                   int32_t* __restrict__ block_base, int row_base,
+                                                   int write_end) {
   __shared__ int total[kMaxE + 1];
   const int e = threadIdx.x;
   if (e < E) {
@@ -67,16 +68,16 @@ __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ b
   if (e < E) {
     const int off = total[e];
     for (int b = 0; b < nblk; ++b) block_base[(size_t)b * E + e] += off;
-    offsets[e] = off;
+    offsets[e] = row_base + off;
     if (counts != nullptr) counts[e] = total[e + 1] - off;
   }
-  if (e == 0) offsets[E] = total[E];
+  if (e == 0 && write_end) offsets[E] = row_base + total[E];
 }
 
 __global__ __launch_bounds__(256) void rank_kernel(const int32_t* __restrict__ idx, int R, int E,
                                                    const int32_t* __restrict__ block_base,
                                                    int32_t* __restrict__ sorted_src,
-                                                   int32_t* __restrict__ row_of) {
+                                                   int32_t* __restrict__ row_of, int row_base) {
   __shared__ int wcnt[kWavesP][kMaxE];
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
@@ -118,7 +119,7 @@ __global__ __launch_bounds__(256) void rank_kernel(const int32_t* __restrict__ i
       if (ok && e == v) {
         const int p = base + __popcll(m & lt_mask);
         sorted_src[p] = f;
-        row_of[f] = p;
+        row_of[f] = row_base + p;
       }
       if (lane == leader) wcnt[wave][v] = base + __popcll(m);
       remaining &= ~m;
@@ -126,17 +127,26 @@ __global__ __launch_bounds__(256) void rank_kernel(const int32_t* __restrict__ i
   }
 }
 
-// Small R: histogram, scan and stable ranks in one workgroup of 16 waves.
-// Wave w owns the contiguous pairs [w*per, (w+1)*per); per-wave counts give
-// every wave its base per expert, then each wave ranks its pairs in flat
-// order with the same ballot walk as rank_kernel.
+// Small R: histogram, scan and stable ranks in one workgroup of 16 waves;
+// workgroup h handles cluster h (ids idx + h*R, outputs at h*R / h*E, rows
+// numbered from row_base = h*R).  Wave w owns the contiguous pairs
+// [w*per, (w+1)*per); per-wave counts give every wave its base per expert,
+// then each wave ranks its pairs in flat order with the same ballot walk as
+// rank_kernel.  The last workgroup writes the final offset.
 constexpr int kSmallWaves = 16;
 constexpr int kSmallMaxR = 8192;
 
 __global__ __launch_bounds__(kSmallWaves * 64) void index_small_kernel(
-    const int32_t* __restrict__ idx, int R, int E, int32_t* __restrict__ counts,
-    int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_src,
-    int32_t* __restrict__ row_of) {
+    const int32_t* __restrict__ idx_all, int R, int E, int32_t* __restrict__ counts_all,
+    int32_t* __restrict__ offsets_all, int32_t* __restrict__ sorted_src_all,
+    int32_t* __restrict__ row_of_all) {
+  const int h = blockIdx.x;
+  const int row_base = h * R;
+  const int32_t* __restrict__ idx = idx_all + (size_t)h * R;
+  int32_t* __restrict__ counts = counts_all != nullptr ? counts_all + (size_t)h * E : nullptr;
+  int32_t* __restrict__ offsets = offsets_all + (size_t)h * E;
+  int32_t* __restrict__ sorted_src = sorted_src_all + (size_t)h * R;
+  int32_t* __restrict__ row_of = row_of_all + (size_t)h * R;
   __shared__ int wcnt[kSmallWaves][kMaxE];
   __shared__ int total[kMaxE + 1];
   const int lane = lane_id();
@@ -171,7 +181,7 @@ __global__ __launch_bounds__(kSmallWaves * 64) void index_small_kernel(
   if (threadIdx.x < E) {
     const int e = threadIdx.x;
     int run = total[e];
-    offsets[e] = run;
+    offsets[e] = row_base + run;
     if (counts != nullptr) counts[e] = total[e + 1] - run;
     for (int w = 0; w < kSmallWaves; ++w) {
       const int c = wcnt[w][e];
@@ -179,7 +189,7 @@ __global__ __launch_bounds__(kSmallWaves * 64) void index_small_kernel(
       run += c;
     }
   }
-  if (threadIdx.x == 0) offsets[E] = total[E];
+  if (threadIdx.x == 0 && h == (int)gridDim.x - 1) offsets[E] = row_base + total[E];
   __syncthreads();
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   for (int f0 = start; f0 < end; f0 += kWave) {
@@ -197,7 +207,7 @@ __global__ __launch_bounds__(kSmallWaves * 64) void index_small_kernel(
       if (ok && e == v) {
         const int p = base + __popcll(m & lt_mask);
         sorted_src[p] = f;
-        row_of[f] = p;
+        row_of[f] = row_base + p;
       }
       if (lane == leader) wcnt[wave][v] = base + __popcll(m);
       remaining &= ~m;
@@ -257,50 +267,62 @@ hipError_t launch_fill_i32(int32_t* p, int n, int32_t v, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_permute(foe_dtype dt, int T, int d, int E, int k, const int32_t* topk_idx,
-                          const void* x, int32_t* counts, int32_t* offsets, int32_t* sorted_src,
-                          int32_t* row_of, void* x_perm, void* scratch, hipStream_t s) {
+hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int32_t* counts,
+                        int32_t* offsets, int32_t* sorted_src, int32_t* row_of, void* scratch,
+                        hipStream_t s) {
   const int R = T * k;
   if (R == 0) {
-    hipError_t err = launch_fill_i32(offsets, E + 1, 0, s);
-    if (err == hipSuccess && counts != nullptr) err = launch_fill_i32(counts, E, 0, s);
+    hipError_t err = launch_fill_i32(offsets, C * E + 1, 0, s);
+    if (err == hipSuccess && counts != nullptr) err = launch_fill_i32(counts, C * E, 0, s);
     return err;
+  }
+  if (R <= kSmallMaxR) {
+    ProfileScope ps("permute_index", s);
+    hipLaunchKernelGGL(index_small_kernel, dim3(C), dim3(kSmallWaves * kWave), 0, s, topk_idx, R,
+                       E, counts, offsets, sorted_src, row_of);
+    return hipGetLastError();
   }
   const int nblk = permute_blocks(R);
   int32_t* block_counts = reinterpret_cast<int32_t*>(scratch);
   int32_t* block_base = block_counts + (size_t)nblk * E;
-  if (R <= kSmallMaxR) {
-    ProfileScope ps("permute_index", s);
-    hipLaunchKernelGGL(index_small_kernel, dim3(1), dim3(kSmallWaves * kWave), 0, s, topk_idx, R,
-                       E, counts, offsets, sorted_src, row_of);
-  } else {
-  {
-    ProfileScope ps("permute_hist", s);
-    hipLaunchKernelGGL(hist_kernel, dim3(nblk), dim3(256), 0, s, topk_idx, R, E, block_counts);
+  for (int h = 0; h < C; ++h) {
+    const int32_t* idx_h = topk_idx + (size_t)h * R;
+    {
+      ProfileScope ps("permute_hist", s);
+      hipLaunchKernelGGL(hist_kernel, dim3(nblk), dim3(256), 0, s, idx_h, R, E, block_counts);
+    }
+    {
+      ProfileScope ps("permute_scan", s);
+      hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(256), 0, s, block_counts, nblk, E,
+                         counts != nullptr ? counts + (size_t)h * E : nullptr,
+                         offsets + (size_t)h * E, block_base, h * R, h == C - 1 ? 1 : 0);
+    }
+    {
+      ProfileScope ps("permute_rank", s);
+      hipLaunchKernelGGL(rank_kernel, dim3(nblk), dim3(256), 0, s, idx_h, R, E, block_base,
+                         sorted_src + (size_t)h * R, row_of + (size_t)h * R, h * R);
+    }
   }
-  {
-    ProfileScope ps("permute_scan", s);
-    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(256), 0, s, block_counts, nblk, E, counts,
-                       offsets, block_base);
-  }
-  {
-    ProfileScope ps("permute_rank", s);
-    hipLaunchKernelGGL(rank_kernel, dim3(nblk), dim3(256), 0, s, topk_idx, R, E, block_base,
-                       sorted_src, row_of);
-  }
-  }
-  {
-    ProfileScope ps("permute_scatter", s);
-    dim3 grid(ceil_div(T, 4));
-    if (dt == FOE_BF16)
-      hipLaunchKernelGGL(scatter_rows_kernel<bf16>, grid, dim3(256), 0, s,
-                         reinterpret_cast<const bf16*>(x), row_of, T, d, k, R,
-                         reinterpret_cast<bf16*>(x_perm));
-    else
-      hipLaunchKernelGGL(scatter_rows_kernel<float>, grid, dim3(256), 0, s,
-                         reinterpret_cast<const float*>(x), row_of, T, d, k, R,
-                         reinterpret_cast<float*>(x_perm));
-  }
+  return hipGetLastError();
+}
+
+hipError_t launch_permute(foe_dtype dt, int T, int d, int E, int k, const int32_t* topk_idx,
+                          const void* x, int32_t* counts, int32_t* offsets, int32_t* sorted_src,
+                          int32_t* row_of, void* x_perm, void* scratch, hipStream_t s) {
+  hipError_t err =
+      launch_index(T, E, k, 1, topk_idx, counts, offsets, sorted_src, row_of, scratch, s);
+  if (err != hipSuccess || T == 0) return err;
+  const int R = T * k;
+  ProfileScope ps("permute_scatter", s);
+  dim3 grid(ceil_div(T, 4));
+  if (dt == FOE_BF16)
+    hipLaunchKernelGGL(scatter_rows_kernel<bf16>, grid, dim3(256), 0, s,
+                       reinterpret_cast<const bf16*>(x), row_of, T, d, k, R,
+                       reinterpret_cast<bf16*>(x_perm));
+  else
+    hipLaunchKernelGGL(scatter_rows_kernel<float>, grid, dim3(256), 0, s,
+                       reinterpret_cast<const float*>(x), row_of, T, d, k, R,
+                       reinterpret_cast<float*>(x_perm));
   return hipGetLastError();
 }
 

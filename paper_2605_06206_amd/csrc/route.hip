@@ -14,7 +14,10 @@ namespace foe {
 namespace {
 
 constexpr int kTok = 16;    // tokens per workgroup
-constexpr int kBatch = 4;   // K steps whose loads are issued together
+#ifndef FOE_ROUTE_BATCH
+#define FOE_ROUTE_BATCH 4
+#endif
+constexpr int kBatch = FOE_ROUTE_BATCH;  // K steps whose loads are issued together
 
 // (v, e) beats (w, f): larger score, equal scores -> lower id
 __device__ __forceinline__ bool beats(float v, int e, float w, int f) {

@@ -373,6 +373,8 @@ def test_block_parity_sampled(name):
     (1, 64, 8, 2, 64, 3, 1.0, "bf16", None),         # one token, literal sum of 3
     (257, 128, 8, 2, 128, 2, None, "bf16", "zipf4"),  # extreme skew: empty experts
     (130, 64, 4, 2, 64, 2, 0.5, "f32", None),
+    (200, 64, 100, 3, 64, 3, None, "bf16", None),    # 300 experts in one grouped FFN
+    (600, 128, 64, 2, 128, 4, None, "bf16", None),    # 256 experts, large-tile path
 ])
 def test_block_parity_shapes(T, d, E, k, F, C, scale, dt, bias):
     say("block shapes", T, d, E, k, F, C, scale, dt, bias)
