@@ -4,6 +4,10 @@
 // fp32 accumulation in a fixed order.
 #include "foe_common.hpp"
 
+#ifndef FOE_COMBINE_U
+#define FOE_COMBINE_U 2
+#endif
+
 namespace foe {
 namespace {
 
@@ -90,7 +94,7 @@ __global__ __launch_bounds__(256) void combine_clusters_kernel(
     const float* __restrict__ w_all, const T* __restrict__ x, int C, int T_, int d, int k,
     int y_rows, float scale, T* __restrict__ out) {
   constexpr int EPV = Vec16<T>::N;
-  constexpr int U = 4;
+  constexpr int U = FOE_COMBINE_U;
   const int lane = lane_id();
   const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (tok >= T_) return;
@@ -103,6 +107,13 @@ __global__ __launch_bounds__(256) void combine_clusters_kernel(
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int e = 0; e < EPV; ++e) acc[u][e] = 0.f;
+    // x does not depend on the routing: issue its loads first
+    Vec16<T> xv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + u * kWave + lane;
+      if (c < nvec) xv[u] = load16(x + (size_t)tok * d + (size_t)c * EPV);
+    }
     for (int h = 0; h < C; ++h) {
       const int32_t* rows = row_of_all + h * R + (size_t)tok * k;
       const float* wts = w_all + h * R + (size_t)tok * k;
@@ -135,10 +146,10 @@ __global__ __launch_bounds__(256) void combine_clusters_kernel(
     for (int u = 0; u < U; ++u) {
       const int c = c0 + u * kWave + lane;
       if (c >= nvec) continue;
-      const Vec16<T> xv = load16(x + (size_t)tok * d + (size_t)c * EPV);
       Vec16<T> o;
 #pragma unroll
-      for (int e = 0; e < EPV; ++e) o.v[e] = from_f32<T>(scale * fmaf(cx, to_f32(xv.v[e]), acc[u][e]));
+      for (int e = 0; e < EPV; ++e)
+        o.v[e] = from_f32<T>(scale * fmaf(cx, to_f32(xv[u].v[e]), acc[u][e]));
       store16(out + (size_t)tok * d + (size_t)c * EPV, o);
     }
   }

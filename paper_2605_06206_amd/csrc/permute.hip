@@ -16,7 +16,7 @@
 namespace foe {
 namespace {
 
-constexpr int kChunk = 2048;            // pairs per block
+constexpr int kChunk = 1024;            // pairs per block
 constexpr int kWavesP = 4;
 constexpr int kPerWave = kChunk / kWavesP;  // 512 pairs per wave
 constexpr int kMaxE = 256;
@@ -37,6 +37,11 @@ __global__ __launch_bounds__(256) void hist_kernel(const int32_t* __restrict__ i
     block_counts[(size_t)blockIdx.x * E + e] = cnt[e];
 }
 
+// Block counts are staged in LDS with coalesced loads (when they fit), so the
+// per-expert prefix over blocks reads LDS instead of a chain of dependent
+// global loads.
+constexpr int kScanStage = 8192;  // int32 entries of block counts staged in LDS
+
 __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ block_counts,
                                                    int nblk, int E,
                                                    int32_t* __restrict__ counts,
@@ -44,17 +49,27 @@ __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ b
                                                    int32_t* __restrict__ block_base, int row_base,
                                                    int write_end) {
   __shared__ int total[kMaxE + 1];
+  __shared__ int staged[kScanStage];
   const int e = threadIdx.x;
+  const int n = nblk * E;
+  const bool stage = n <= kScanStage;
+  if (stage)
+    for (int i = threadIdx.x; i < n; i += blockDim.x) staged[i] = block_counts[i];
+  __syncthreads();
   if (e < E) {
     int run = 0;
     for (int b = 0; b < nblk; ++b) {
-      block_base[(size_t)b * E + e] = run;
-      run += block_counts[(size_t)b * E + e];
+      const int c = stage ? staged[b * E + e] : block_counts[(size_t)b * E + e];
+      if (stage)
+        staged[b * E + e] = run;
+      else
+        block_base[(size_t)b * E + e] = run;
+      run += c;
     }
     total[e] = run;
   }
   __syncthreads();
-  // exclusive prefix over experts, written in place as offsets (E <= 256)
+  // exclusive prefix over experts (E <= 256)
   if (threadIdx.x == 0) {
     int run = 0;
     for (int i = 0; i < E; ++i) {
@@ -67,11 +82,16 @@ __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ b
   __syncthreads();
   if (e < E) {
     const int off = total[e];
-    for (int b = 0; b < nblk; ++b) block_base[(size_t)b * E + e] += off;
     offsets[e] = row_base + off;
     if (counts != nullptr) counts[e] = total[e + 1] - off;
   }
   if (e == 0 && write_end) offsets[E] = row_base + total[E];
+  // block bases (coalesced stores)
+  if (stage) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x) block_base[i] = staged[i] + total[i % E];
+  } else if (e < E) {
+    for (int b = 0; b < nblk; ++b) block_base[(size_t)b * E + e] += total[e];
+  }
 }
 
 __global__ __launch_bounds__(256) void rank_kernel(const int32_t* __restrict__ idx, int R, int E,
