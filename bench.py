@@ -11,6 +11,12 @@ Default workload: the decode-shaped cluster block (T=128, d=2048, E=16, k=2,
 F=1024, bf16).  Several independent weight/input sets are rotated so the
 working set exceeds the 256 MB Infinity Cache.
 
+`traffic` in the roofline object is the measured HBM traffic per launch of the
+dominant kernel (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by what the same
+counters read for a plain copy of known size: `--copy-calibration`), read from
+profiles/traffic.json; it is null when no measurement exists for this
+workload or the kernel's source has changed since it was taken.
+
 Timed passes (both over K steps, HIP events on the library's stream):
   A  plain steps -> value / ms_per_step (replayed from HIP graphs unless
      --no-graph; the eager time is reported beside it)
@@ -48,7 +54,50 @@ def parse():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the oracle CPU baseline (0 = skip)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy 10 times (reference for "
+                         "rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     return ap.parse_args()
+
+
+# kernel name (library timing hooks) -> source file that holds it
+KERNEL_SOURCES = {"route": "route.hip", "index": "permute.hip", "permute": "permute.hip",
+                  "ffn_gateup": "ffn.hip", "ffn_down": "ffn.hip", "ffn_gateup_f32": "ffn.hip",
+                  "ffn_down_f32": "ffn.hip", "combine": "combine.hip", "reduce": "combine.hip"}
+
+
+def source_sha(kernel):
+    import hashlib
+    src = KERNEL_SOURCES.get(kernel)
+    if src is None:
+        return None
+    path = os.path.join(ROOT, "paper_2605_06206_amd", "csrc", src)
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(config, kernel):
+    """HBM bytes per launch measured with rocprofv3 counters for this workload
+    and kernel, or None (no record, or the kernel source changed since)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f).get(config, {}).get(kernel)
+    if not rec or rec.get("source_sha256") != source_sha(kernel):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def copy_calibration():
+    import torch
+    n = 1 << 30
+    src = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 10}), flush=True)
 
 
 def kernel_work(name, cfg, e_touched):
@@ -122,6 +171,9 @@ def cpu_baseline(cfg_name, budget_s):
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the per-cluster block has no multi-GPU path in "
               "this build (use --gpus 1)", file=sys.stderr)
@@ -241,6 +293,7 @@ def main():
     foe.profile_reset()
     dom = max(kernels, key=lambda n: kernels[n]["total_ms"])
     roof = roofline(dom, cfg, e_touched, kernels[dom]["avg_us"] * 1e-6)
+    roof["traffic"] = measured_traffic(args.config, dom)
     per_kernel_roof = {n: roofline(n, cfg, e_touched, v["avg_us"] * 1e-6)
                        for n, v in kernels.items() if kernel_work(n, cfg, e_touched)[1] > 0}
 

@@ -36,6 +36,17 @@
 #ifndef FOE_SKINNY
 #define FOE_SKINNY 4, 4
 #endif
+// LDS-DMA large-M kernel: on/off; (BM, BN, WM, WN, BK, LDS stages, L2
+// prefetch distance in stages, M-tile group of the tile order, persistent)
+#ifndef FOE_GEMM_DMA
+#define FOE_GEMM_DMA 1
+#endif
+#ifndef FOE_DMA_GU
+#define FOE_DMA_GU 256, 128, 2, 4, 64, 2, 0, 4, 1
+#endif
+#ifndef FOE_DMA_DN
+#define FOE_DMA_DN 256, 256, 2, 4, 64, 2, 0, 4, 1
+#endif
 
 namespace foe {
 namespace {
@@ -375,6 +386,356 @@ void grouped_gemm_bf16(const bf16* __restrict__ A, const int32_t* __restrict__ g
   }
 }
 
+// ---- LDS-DMA variant of the large-M grouped GEMM ---------------------------
+// Operand tiles go from global memory straight into LDS with
+// `buffer_load_dwordx4 ... lds`: each lane of a wave deposits 16 bytes at
+// M0 + 16 * lane, so one instruction fills 1 KiB of LDS and the tile never
+// passes through VGPRs (no ds_write, no staging registers).  The loads are
+// issued from inline assembly so that their completion is tracked here with
+// explicit vmcnt waits (the compiler does not see them; the kernel issues no
+// other global loads inside the main loop and uses M0 nowhere else).
+//
+// LDS layout of a tile: rows of BK bf16 (no padding), the 16-byte chunk c of
+// row r stored in slot c ^ swz(r).  A fragment read (32 rows, one chunk) then
+// touches every bank group once per 16 lanes.  Since a DMA instruction
+// writes 1 KiB contiguously, the swizzle is applied on the load side: the
+// lane that lands in slot s of row r fetches chunk s ^ swz(r).
+// LDS byte address of a __shared__ object: a generic address in the LDS
+// aperture carries the aperture in its high 32 bits and the LDS offset in its
+// low 32 bits (taking the low half avoids the null check of an address-space
+// cast).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+// Buffer resource built from wave-uniform (readfirstlane) fields, so that it
+// is guaranteed to sit in SGPRs as the inline assembly below requires.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc_u(const void* base, uint32_t nbytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  void* p = (void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, __builtin_amdgcn_readfirstlane(nbytes),
+                                           0x00020000);
+}
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(r),
+               "s"(lds)
+               : "memory");
+}
+// wait until at most N of this wave's global loads are outstanding and its
+// LDS reads are done, then meet the other waves
+template <int N>
+__device__ __forceinline__ void vm_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+template <int CPR>
+__device__ __forceinline__ int swz(int r) {
+  static_assert(CPR == 4 || CPR == 8, "rows of 64 or 128 bytes");
+  if constexpr (CPR == 8) return (r & 7) ^ ((r >> 3) & 1);
+  else return ((r >> 1) & 3) ^ ((r >> 3) & 1);
+}
+
+template <int BM, int BN, int WM, int WN, bool GATEUP, int BK, int NST, int PF>
+struct DmaCfg {
+  static constexpr int NW = WM * WN, NTHR = NW * kWave;
+  static constexpr int WTM = BM / WM, WTN = BN / WN;
+  static constexpr int SM = WTM / 32, SN = WTN / 32;
+  static constexpr int NB = GATEUP ? 2 : 1;
+  static constexpr int RB = BK * 2;        // bytes per tile row
+  static constexpr int CPR = BK / 8;       // 16-byte chunks per row
+  static constexpr int RPI = 1024 / RB;    // rows per DMA instruction
+  static constexpr int A_PER = BM / RPI / NW, B_PER = BN / RPI / NW;  // per wave
+  static constexpr int NLD = A_PER + NB * B_PER;
+  static constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB;
+  static constexpr int STAGE = A_BYTES + NB * B_BYTES;
+  static constexpr int KS = BK / 16;       // k16 steps per stage
+  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be a multiple of 32");
+  static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "even DMA split");
+  static_assert(KS % 2 == 0, "fragment slots alternate within a stage");
+  static_assert(NST >= 2 && NLD * (NST - 2) <= 63, "vmcnt range");
+  static_assert(NST * STAGE + 1024 <= 160 * 1024, "LDS capacity");
+  // L2 prefetch PF stages ahead of the DMA: one 16-byte touch per 128-byte
+  // tile row segment, one instruction per wave (rows of a wave share a tile)
+  static_assert(PF == 0 || (NST == 2 && BK == 64 && BM + NB * BN == NTHR && BM % kWave == 0 &&
+                            BN % kWave == 0),
+                "prefetch layout: one tile row per thread");
+};
+
+// Stage kt (K columns kt*BK ..) lives in LDS buffer kt % NST.  Iteration kt:
+//   issue the DMA of stage kt+NST-1 into the buffer freed by stage kt-1 (and,
+//   with PF > 0, touch the rows of stage kt+NST-1+PF so that they are in L2
+//   when their DMA comes: a stage's DMA then has an iteration to complete
+//   against L2 latency rather than HBM latency);
+//   k16 steps 0..KS-2 of stage kt (fragment reads one step ahead);
+//   wait for stage kt+1 and meet the other waves;
+//   read the first fragments of stage kt+1; k16 step KS-1 of stage kt.
+template <int BM, int BN, int WM, int WN, bool GATEUP, int BK, int NST, int PF, int GM,
+          bool PERSIST>
+__global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1, 2)))
+void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv,
+                      int a_rows, const int32_t* __restrict__ offsets, int E, int rows,
+                      const bf16* __restrict__ B0, const bf16* __restrict__ B1, int N, int K,
+                      bf16* __restrict__ out, int n_tiles_n, int n_tiles) {
+  using C = DmaCfg<BM, BN, WM, WN, GATEUP, BK, NST, PF>;
+  constexpr int NLD = C::NLD;
+  // NST stages, then 1 KiB that absorbs the data of the prefetch touches
+  __shared__ __align__(1024) unsigned char smem[NST * C::STAGE + 1024];
+
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+
+  auto run_tile = [&](const int e, const int row0, const int row_end, const int ntile) {
+    const int n0 = ntile * BN;
+
+    const int n_valid = min(BN, N - n0);
+    // operand ranges: A rows (a per-tile range, or the whole source when
+    // gathering), then one weight slice per matrix
+    const bf16* t_base[1 + C::NB];
+    uint32_t t_bytes[1 + C::NB];
+    t_base[0] = gather == nullptr ? A + (size_t)row0 * K : A;
+    t_bytes[0] = gather == nullptr ? (uint32_t)min(BM, row_end - row0) * K * 2u
+                                   : (uint32_t)a_rows * K * 2u;
+    t_base[1] = B0 + ((size_t)e * N + n0) * K;
+    t_bytes[1] = (uint32_t)n_valid * K * 2u;
+    if constexpr (GATEUP) {
+      t_base[2] = B1 + ((size_t)e * N + n0) * K;
+      t_bytes[2] = t_bytes[1];
+    }
+    __amdgpu_buffer_rsrc_t rsrc[1 + C::NB];
+#pragma unroll
+    for (int t = 0; t <= C::NB; ++t) rsrc[t] = make_rsrc_u(t_base[t], t_bytes[t]);
+
+    // DMA instruction q of this wave: source byte offset inside the K slab
+    // (kOob: reads zeros), k of its chunk, LDS offset inside a stage
+    uint32_t g_off[NLD], l_dst[NLD];
+    int g_k[NLD];
+#pragma unroll
+    for (int q = 0; q < NLD; ++q) {
+      const bool is_a = q < C::A_PER;
+      const int jj = is_a ? q : q - C::A_PER;
+      const int tb = is_a ? 0 : 1 + jj / C::B_PER;
+      const int ii = wave * (is_a ? C::A_PER : C::B_PER) + (is_a ? jj : jj % C::B_PER);
+      const int r = ii * C::RPI + lane / C::CPR;
+      const int c = (lane % C::CPR) ^ swz<C::CPR>(r);
+      g_k[q] = c * 8;
+      l_dst[q] = __builtin_amdgcn_readfirstlane((tb == 0 ? 0 : C::A_BYTES + (tb - 1) * C::B_BYTES) +
+                                                ii * 1024);
+      if (is_a) {
+        if (gather == nullptr) {
+          g_off[q] = (uint32_t)(r * K + c * 8) * 2u;
+        } else {
+          const int s = (row0 + r < row_end) ? src_row(gather, kdiv, row0 + r, a_rows) : -1;
+          g_off[q] = s < 0 ? kOob : ((uint32_t)s * K + c * 8) * 2u;
+        }
+      } else {
+        g_off[q] = (uint32_t)(r * K + c * 8) * 2u;
+      }
+    }
+    const uint32_t smem_base = lds_addr(smem);
+    // prefetch row of this thread: tile (wave-uniform) and byte offset of the row
+    const int pf_t = __builtin_amdgcn_readfirstlane(tid < BM ? 0 : 1 + (tid - BM) / BN);
+    uint32_t pf_off = kOob;
+    if constexpr (PF > 0) {
+      const int pr = tid < BM ? tid : (tid - BM) % BN;
+      if (pf_t > 0 || gather == nullptr) {
+        pf_off = (uint32_t)pr * K * 2u;
+      } else {
+        const int s = (row0 + pr < row_end) ? src_row(gather, kdiv, row0 + pr, a_rows) : -1;
+        pf_off = s < 0 ? kOob : (uint32_t)s * K * 2u;
+      }
+    }
+    const __amdgpu_buffer_rsrc_t rsrc_pf = make_rsrc_u(
+        pf_t == 0 ? t_base[0] : (pf_t == 1 ? t_base[1] : t_base[C::NB]),
+        pf_t == 0 ? t_bytes[0] : (pf_t == 1 ? t_bytes[1] : t_bytes[C::NB]));
+    const uint32_t junk = __builtin_amdgcn_readfirstlane(lds_addr(smem + NST * C::STAGE));
+    const int nk_real = (K + BK - 1) / BK;
+    auto prefetch = [&](int kt) {
+      const bool ok = pf_off != kOob && kt < nk_real;
+      dma16(rsrc_pf, ok ? pf_off + (uint32_t)kt * BK * 2u : kOob, junk);
+    };
+    // DMA instruction q of stage kt into LDS buffer buf (stages past K read zeros)
+    auto issue_one = [&](int kt, int buf, int q) {
+      const bool is_a = q < C::A_PER;
+      const __amdgpu_buffer_rsrc_t r = is_a ? rsrc[0] : rsrc[1 + (q - C::A_PER) / C::B_PER];
+      const int k0 = kt * BK;
+      const uint32_t voff =
+          (k0 + g_k[q] < K && g_off[q] != kOob) ? g_off[q] + (uint32_t)k0 * 2u : kOob;
+      dma16(r, voff, smem_base + (uint32_t)buf * C::STAGE + l_dst[q]);
+    };
+
+    f32x16 acc[C::NB][C::SM][C::SN];
+#pragma unroll
+    for (int b = 0; b < C::NB; ++b)
+#pragma unroll
+      for (int i = 0; i < C::SM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::SN; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) acc[b][i][j][v] = 0.f;
+
+    // fragment rows are congruent to lane%32 modulo 32, so one swizzle per lane
+    const int lrow = lane & 31;
+    const int sw = swz<C::CPR>(lrow) ^ (lane >> 5);
+    int xo[C::KS];
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) xo[ks] = ((2 * ks) ^ sw) * 16;
+    const int a_row = (wm * C::WTM + lrow) * C::RB;
+    const int b_row = C::A_BYTES + (wn * C::WTN + lrow) * C::RB;
+    bf16x8 xa[2][C::SM];
+    bf16x8 wf[2][C::NB][C::SN];
+    auto fload = [&](int buf, int ks, int slot) {
+      const unsigned char* sa = smem + buf * C::STAGE;
+#pragma unroll
+      for (int i = 0; i < C::SM; ++i)
+        xa[slot][i] = *reinterpret_cast<const bf16x8*>(sa + a_row + xo[ks] + i * 32 * C::RB);
+#pragma unroll
+      for (int b = 0; b < C::NB; ++b)
+#pragma unroll
+        for (int j = 0; j < C::SN; ++j)
+          wf[slot][b][j] = *reinterpret_cast<const bf16x8*>(sa + b_row + xo[ks] + b * C::B_BYTES +
+                                                            j * 32 * C::RB);
+    };
+    constexpr int NM = C::NB * C::SM * C::SN;  // MFMAs per k16 step
+    constexpr int NR = C::SM + C::NB * C::SN;  // fragment reads per k16 step
+    static_assert(NR <= NM, "one fragment read per MFMA");
+    // One k16 step in a fixed order: MFMA t of fragment slot `slot`, then
+    // fragment read t of (rbuf, rks) into the other slot (rks >= 0), then the
+    // DMA instructions [q0, q1) of stage dkt (buffer dbuf) spread evenly over
+    // the MFMAs, and the prefetch of stage pkt (>= 0) after the last MFMA.  A
+    // burst of DMA instructions would stall the wave on the address queue
+    // while its MFMA pipe drains; spread out, the queue drains under the MFMAs.
+    auto kstep = [&](int slot, int rbuf, int rks, int dkt, int dbuf, int q0, int q1, int pkt) {
+      const unsigned char* sa = smem + rbuf * C::STAGE;
+#pragma unroll
+      for (int t = 0; t < NM; ++t) {
+        const int b = t / (C::SN * C::SM), j = (t / C::SM) % C::SN, i = t % C::SM;
+        acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[slot][b][j], xa[slot][i],
+                                                               acc[b][i][j], 0, 0, 0);
+        if (rks >= 0 && t < NR) {
+          if (t < C::SM) {
+            xa[slot ^ 1][t] =
+                *reinterpret_cast<const bf16x8*>(sa + a_row + xo[rks] + t * 32 * C::RB);
+          } else {
+            const int u = t - C::SM, ub = u / C::SN, uj = u % C::SN;
+            wf[slot ^ 1][ub][uj] = *reinterpret_cast<const bf16x8*>(
+                sa + b_row + xo[rks] + ub * C::B_BYTES + uj * 32 * C::RB);
+          }
+        }
+#pragma unroll
+        for (int q = q0; q < q1; ++q)
+          if ((q - q0) * NM / (q1 - q0) == t) issue_one(dkt, dbuf, q);
+        if (t == NM - 1 && pkt >= 0) prefetch(pkt);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+
+    // K steps rounded up to a multiple of NST: steps past K read zeros.
+    // The DMA of stage kt+NST-1 is spread over the k16 steps of iteration kt:
+    // with two stages it must be complete at this iteration's barrier, so it
+    // goes out in the first KS-2 steps (at least one); with more stages it may
+    // use every step.  DS = steps carrying DMA, Q(s) = first instruction of
+    // step s, BEFORE = instructions issued before the barrier.
+    const int nk = ((K + BK - 1) / BK + NST - 1) / NST * NST;
+    constexpr int KS = C::KS;
+    constexpr int DS = NST == 2 ? (KS - 2 > 1 ? KS - 2 : 1) : KS;
+    constexpr int BEFORE = NST == 2 ? NLD : (KS - 1) * NLD / KS;
+    // loads allowed in flight at the barrier of iteration kt (stage kt+1
+    // complete): the later stages' DMAs issued so far and the prefetch
+    constexpr int VM_AT_BARRIER =
+        NST == 2 ? (PF > 0 ? 1 : 0) : (NST - 3) * NLD + BEFORE;
+    static_assert(VM_AT_BARRIER <= 63, "vmcnt range");
+    auto qof = [&](int st) { return st >= DS ? NLD : st * NLD / DS; };
+    auto iteration = [&](int kt, int b) {
+      const int dkt = kt + NST - 1, dbuf = (b + NST - 1) % NST;
+      const int pkt = PF > 0 ? kt + 1 + PF : -1;
+#pragma unroll
+      for (int st = 0; st + 1 < KS; ++st)
+        kstep(st & 1, b, st + 1, dkt, dbuf, qof(st), qof(st + 1),
+              st == (DS < KS - 1 ? DS : KS - 1) - 1 ? pkt : -1);
+      vm_barrier<VM_AT_BARRIER>();
+      kstep((KS - 1) & 1, (b + 1) % NST, 0, dkt, dbuf, qof(KS - 1), qof(KS), -1);
+    };
+
+#pragma unroll
+    for (int st = 0; st < NST - 1; ++st)
+#pragma unroll
+      for (int q = 0; q < NLD; ++q) issue_one(st, st, q);
+    if constexpr (PF > 0) {
+#pragma unroll
+      for (int st = 1; st <= PF; ++st) prefetch(st);
+      vm_barrier<PF>();
+    } else {
+      vm_barrier<NLD * (NST - 2)>();
+    }
+    fload(0, 0, 0);
+    for (int kt = 0; kt < nk; kt += NST) {
+#pragma unroll
+      for (int u = 0; u < NST; ++u) iteration(kt + u, u);
+    }
+    // the last DMAs (zeros past K) land before the buffers are reused
+    vm_barrier<0>();
+
+    // epilogue: lane holds row m = .. + lane%32, columns n = .. + 8q + 4*(lane/32) + [0,4)
+#pragma unroll
+    for (int i = 0; i < C::SM; ++i) {
+      const int m = row0 + wm * C::WTM + i * 32 + lrow;
+      if (m >= row_end) continue;
+#pragma unroll
+      for (int j = 0; j < C::SN; ++j) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int n = n0 + wn * C::WTN + j * 32 + q * 8 + (lane >> 5) * 4;
+          if (n >= N) continue;
+          bf16x4 o;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            float val = acc[0][i][j][q * 4 + v];
+            if constexpr (GATEUP) val = silu_f(val) * acc[C::NB - 1][i][j][q * 4 + v];
+            o[v] = (bf16)val;
+          }
+          *reinterpret_cast<bf16x4*>(out + (size_t)m * N + n) = o;
+        }
+      }
+    }
+  };
+
+  // tile t -> (M-tile, N-tile): groups of GM M-tiles are walked N-tile by
+  // N-tile, so that a run of consecutive tiles shares A rows and weight slices
+  auto tile_coords = [&](int t, int& mt, int& nt) {
+    if constexpr (GM <= 1) {
+      mt = t / n_tiles_n;
+      nt = t % n_tiles_n;
+    } else {
+      // the last group may hold fewer than GM M-tiles
+      const int grp = t / (GM * n_tiles_n), i = t % (GM * n_tiles_n);
+      const int g = min(GM, n_tiles / n_tiles_n - grp * GM);
+      mt = grp * GM + i % g;
+      nt = i / g;
+    }
+  };
+  if constexpr (PERSIST) {
+    // one workgroup per CU; the workgroups of an XCD take its tile range in
+    // rounds, so the tiles that share operands run side by side
+    constexpr int kXcd = 8;
+    const int x = blockIdx.x % kXcd, l = blockIdx.x / kXcd, nl = gridDim.x / kXcd;
+    const int per = (n_tiles + kXcd - 1) / kXcd;
+    for (int q = l; q < per && x * per + q < n_tiles; q += nl) {
+      int mt, nt, e, row0, row_end;
+      tile_coords(x * per + q, mt, nt);
+      if (!find_tile(offsets, E, rows, BM, mt, e, row0, row_end)) continue;
+      vm_barrier<0>();  // the previous tile's LDS reads are done everywhere
+      run_tile(e, row0, row_end, nt);
+    }
+  } else {
+    const int tile = xcd_tile(blockIdx.x, gridDim.x);
+    if (tile >= n_tiles) return;
+    int mt, nt, e, row0, row_end;
+    tile_coords(tile, mt, nt);
+    if (!find_tile(offsets, E, rows, BM, mt, e, row0, row_end)) return;
+    run_tile(e, row0, row_end, nt);
+  }
+}
+
 // Few rows per expert (decode): the FFN is a weight stream.  A workgroup owns
 // one expert and a slice of weight rows (16 gate + 16 up rows, or 32 down
 // rows); its KW waves split K and read the weights with 128-bit buffer loads
@@ -559,6 +920,42 @@ void launch_gemm(const bf16* A, const int32_t* gather, int kdiv, int a_rows,
                      B1, N, K, out, ntn, (int)n_tiles);
 }
 
+// compute units of the current device (one persistent workgroup each)
+int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 8)
+    return 256;
+  return n / 8 * 8;
+}
+
+template <int BM, int BN, int WM, int WN, int BK, int NST, int PF, int GM, int PERSIST, bool GATEUP>
+void launch_gemm_dma(const bf16* A, const int32_t* gather, int kdiv, int a_rows,
+                     const int32_t* offsets, int E, int rows, const bf16* B0, const bf16* B1,
+                     int N, int K, bf16* out, hipStream_t s, const char* name) {
+  const int ntn = ceil_div(N, BN);
+  const int max_mt = ceil_div(rows, BM) + E;  // sum_e ceil(M_e/BM) <= rows/BM + E
+  const long long n_tiles = (long long)max_mt * ntn;
+  long long nb = (n_tiles + 7) / 8 * 8;
+  if (PERSIST) {
+    static const int cus = device_cus();
+    nb = nb < cus ? nb : cus;
+  }
+  dim3 grid((unsigned)nb);
+  ProfileScope ps(name, s);
+  hipLaunchKernelGGL((grouped_gemm_dma<BM, BN, WM, WN, GATEUP, BK, NST, PF, GM, PERSIST != 0>), grid,
+                     dim3(WM * WN * kWave), 0, s, A, gather, kdiv, a_rows, offsets, E, rows, B0,
+                     B1, N, K, out, ntn, (int)n_tiles);
+}
+
+template <int BM, int BN, int WM, int WN, int BK, int NST, int PF, int GM, int PERSIST>
+struct DmaLaunch {
+  template <bool GATEUP, typename... Args>
+  static void run(Args... args) {
+    launch_gemm_dma<BM, BN, WM, WN, BK, NST, PF, GM, PERSIST, GATEUP>(args...);
+  }
+};
+
 }  // namespace
 
 size_t ffn_scratch_bytes(foe_dtype dt, int rows, int F) {
@@ -609,10 +1006,18 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
                          wd, nullptr, d, F, y, ng);
     }
   } else {
+#if FOE_GEMM_DMA
+    DmaLaunch<FOE_DMA_GU>::run<true>(xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F, d, h,
+                                     s, "ffn_gateup");
+    DmaLaunch<FOE_DMA_DN>::run<false>(static_cast<const bf16*>(h), (const int32_t*)nullptr, 1,
+                                      rows, offsets, E, rows, wd, (const bf16*)nullptr, d, F, y, s,
+                                      "ffn_down");
+#else
     launch_gemm<FOE_PIPE_GU, true, FOE_PIPE_OPT>(xa, gather, kdiv, a_rows, offsets, E, rows, wg,
                                                  wu, F, d, h, s, "ffn_gateup");
     launch_gemm<FOE_PIPE_DN, false, FOE_PIPE_OPT>(h, nullptr, 1, rows, offsets, E, rows, wd,
                                                   nullptr, d, F, y, s, "ffn_down");
+#endif
   }
   return hipGetLastError();
 }
