@@ -19,6 +19,8 @@
 //
 // bf16, few rows per expert (decode, weight-streaming bound): see
 // ffn_skinny_bf16.  fp32: plain FMA kernels (small shapes only).
+#include <type_traits>
+
 #include "foe_common.hpp"
 
 // (BM, BN per weight matrix, waves along M, waves along N) of the large-M
@@ -36,16 +38,16 @@
 #ifndef FOE_SKINNY
 #define FOE_SKINNY 4, 4
 #endif
-// LDS-DMA large-M kernel: on/off; (BM, BN, WM, WN, BK, LDS stages, L2
-// prefetch distance in stages, M-tile group of the tile order, persistent)
+// LDS-DMA large-M kernel: on/off; (BM, BN, WM, WN, BK, LDS stages, waves that
+// issue the DMA (0 = all), M-tile group of the tile order, persistent)
 #ifndef FOE_GEMM_DMA
 #define FOE_GEMM_DMA 1
 #endif
 #ifndef FOE_DMA_GU
-#define FOE_DMA_GU 256, 128, 2, 4, 64, 2, 0, 4, 1
+#define FOE_DMA_GU 256, 128, 2, 4, 64, 2, 4, 4, 1
 #endif
 #ifndef FOE_DMA_DN
-#define FOE_DMA_DN 256, 256, 2, 4, 64, 2, 0, 4, 1
+#define FOE_DMA_DN 256, 256, 2, 4, 64, 2, 4, 4, 1
 #endif
 
 namespace foe {
@@ -139,7 +141,7 @@ __device__ __forceinline__ int src_row(const int32_t* __restrict__ gather, int k
 // tile index is remapped so that each XCD walks a contiguous range of tiles:
 // neighbouring tiles share their A rows (same M-tile) or their weight slice
 // (same expert), and now meet in the same L2.
-__device__ __forceinline__ int xcd_tile(int bid, int nblocks) {
+[[maybe_unused]] __device__ __forceinline__ int xcd_tile(int bid, int nblocks) {
   constexpr int kXcd = 8;
   const int per = (nblocks + kXcd - 1) / kXcd;
   return (bid % kXcd) * per + bid / kXcd;
@@ -148,7 +150,7 @@ __device__ __forceinline__ int xcd_tile(int bid, int nblocks) {
 // LDS-only workgroup barrier: waits for this wave's LDS operations and meets
 // the other waves, but (unlike __syncthreads) does not drain outstanding
 // global loads, so prefetches stay in flight across it.
-__device__ __forceinline__ void lds_barrier() {
+[[maybe_unused]] __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
@@ -415,9 +417,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc_u(const void* base, 
   return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, __builtin_amdgcn_readfirstlane(nbytes),
                                            0x00020000);
 }
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(r),
-               "s"(lds)
+// LDS destination = lds + imm; imm is a constant once the call is inlined
+// (the library is built with optimisation), so the per-instruction LDS
+// addresses cost no registers.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds,
+                                      int imm) {
+  asm volatile("s_add_u32 m0, %2, %3\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff),
+               "s"(r), "s"(lds), "i"(imm)
                : "memory");
 }
 // wait until at most N of this wave's global loads are outstanding and its
@@ -433,56 +439,59 @@ __device__ __forceinline__ int swz(int r) {
   else return ((r >> 1) & 3) ^ ((r >> 3) & 1);
 }
 
-template <int BM, int BN, int WM, int WN, bool GATEUP, int BK, int NST, int PF>
+template <int BM, int BN, int WM, int WN, bool GATEUP, int BK, int NST, int PW>
 struct DmaCfg {
   static constexpr int NW = WM * WN, NTHR = NW * kWave;
+  static constexpr int NP = PW > 0 ? PW : NW;  // waves that issue the DMA
   static constexpr int WTM = BM / WM, WTN = BN / WN;
   static constexpr int SM = WTM / 32, SN = WTN / 32;
   static constexpr int NB = GATEUP ? 2 : 1;
   static constexpr int RB = BK * 2;        // bytes per tile row
   static constexpr int CPR = BK / 8;       // 16-byte chunks per row
   static constexpr int RPI = 1024 / RB;    // rows per DMA instruction
-  static constexpr int A_PER = BM / RPI / NW, B_PER = BN / RPI / NW;  // per wave
-  static constexpr int NLD = A_PER + NB * B_PER;
+  static constexpr int A_INS = BM / RPI, B_INS = BN / RPI;  // DMA instructions per tile
+  static constexpr int NLD = (A_INS + NB * B_INS) / NP;      // per issuing wave
   static constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB;
   static constexpr int STAGE = A_BYTES + NB * B_BYTES;
   static constexpr int KS = BK / 16;       // k16 steps per stage
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be a multiple of 32");
-  static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "even DMA split");
+  static_assert(BM % RPI == 0 && BN % RPI == 0 && (A_INS + NB * B_INS) % NP == 0 && NP <= NW,
+                "even DMA split");
+  // the instructions of an issuing wave stay inside one tile, and the row
+  // parity that selects the swizzle follows the instruction index
+  static_assert(A_INS % NLD == 0 && B_INS % NLD == 0 && (NLD * RPI / 8) % 2 == 0,
+                "one tile per issuing wave");
   static_assert(KS % 2 == 0, "fragment slots alternate within a stage");
   static_assert(NST >= 2 && NLD * (NST - 2) <= 63, "vmcnt range");
-  static_assert(NST * STAGE + 1024 <= 160 * 1024, "LDS capacity");
-  // L2 prefetch PF stages ahead of the DMA: one 16-byte touch per 128-byte
-  // tile row segment, one instruction per wave (rows of a wave share a tile)
-  static_assert(PF == 0 || (NST == 2 && BK == 64 && BM + NB * BN == NTHR && BM % kWave == 0 &&
-                            BN % kWave == 0),
-                "prefetch layout: one tile row per thread");
+  static_assert(NST * STAGE <= 160 * 1024, "LDS capacity");
 };
 
 // Stage kt (K columns kt*BK ..) lives in LDS buffer kt % NST.  Iteration kt:
-//   issue the DMA of stage kt+NST-1 into the buffer freed by stage kt-1 (and,
-//   with PF > 0, touch the rows of stage kt+NST-1+PF so that they are in L2
-//   when their DMA comes: a stage's DMA then has an iteration to complete
-//   against L2 latency rather than HBM latency);
+//   issue the DMA of stage kt+NST-1 into the buffer freed by stage kt-1;
 //   k16 steps 0..KS-2 of stage kt (fragment reads one step ahead);
 //   wait for stage kt+1 and meet the other waves;
 //   read the first fragments of stage kt+1; k16 step KS-1 of stage kt.
-template <int BM, int BN, int WM, int WN, bool GATEUP, int BK, int NST, int PF, int GM,
+// Only the first PW waves (one per SIMD when PW = 4) issue DMA instructions.
+// The address unit of a CU takes a stage's instructions at a fixed rate, and
+// a wave whose instruction finds its queue full stops issuing; when every
+// wave loads, both waves of a SIMD stall together and its MFMA pipe idles.
+// With producer waves, the other wave of each SIMD keeps issuing MFMAs.
+template <int BM, int BN, int WM, int WN, bool GATEUP, int BK, int NST, int PW, int GM,
           bool PERSIST>
 __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv,
                       int a_rows, const int32_t* __restrict__ offsets, int E, int rows,
                       const bf16* __restrict__ B0, const bf16* __restrict__ B1, int N, int K,
                       bf16* __restrict__ out, int n_tiles_n, int n_tiles) {
-  using C = DmaCfg<BM, BN, WM, WN, GATEUP, BK, NST, PF>;
+  using C = DmaCfg<BM, BN, WM, WN, GATEUP, BK, NST, PW>;
   constexpr int NLD = C::NLD;
-  // NST stages, then 1 KiB that absorbs the data of the prefetch touches
-  __shared__ __align__(1024) unsigned char smem[NST * C::STAGE + 1024];
+  __shared__ __align__(1024) unsigned char smem[NST * C::STAGE];
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
 
   auto run_tile = [&](const int e, const int row0, const int row_end, const int ntile) {
     const int n0 = ntile * BN;
@@ -501,66 +510,53 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
       t_base[2] = B1 + ((size_t)e * N + n0) * K;
       t_bytes[2] = t_bytes[1];
     }
-    __amdgpu_buffer_rsrc_t rsrc[1 + C::NB];
-#pragma unroll
-    for (int t = 0; t <= C::NB; ++t) rsrc[t] = make_rsrc_u(t_base[t], t_bytes[t]);
 
-    // DMA instruction q of this wave: source byte offset inside the K slab
-    // (kOob: reads zeros), k of its chunk, LDS offset inside a stage
-    uint32_t g_off[NLD], l_dst[NLD];
-    int g_k[NLD];
+    // Issuing wave p loads instructions p*NLD .. p*NLD+NLD-1 of the stage (A
+    // tile first, then each weight tile; 1 KiB = RPI rows each), all inside
+    // tile tw starting at its instruction ii0.  Lane l lands in row rl = l/CPR,
+    // slot l%CPR of an instruction's rows and so fetches chunk
+    // (l%CPR) ^ swz(row); the swizzle depends on the instruction only through
+    // the parity of its first row / 8, so each lane keeps two chunk choices.
+    // Gathered A rows keep one source offset per instruction.
+    const int p = min(wave_u, C::NP - 1);
+    const int tw = p * NLD < C::A_INS ? 0 : 1 + (p * NLD - C::A_INS) / C::B_INS;
+    const int ii0 = tw == 0 ? p * NLD : (p * NLD - C::A_INS) % C::B_INS;
+    const __amdgpu_buffer_rsrc_t rsrc_w =
+        make_rsrc_u(tw == 0 ? t_base[0] : (tw == 1 ? t_base[1] : t_base[C::NB]),
+                    tw == 0 ? t_bytes[0] : (tw == 1 ? t_bytes[1] : t_bytes[C::NB]));
+    const uint32_t lds_w = (tw == 0 ? 0 : C::A_BYTES + (tw - 1) * C::B_BYTES) + ii0 * 1024;
+    const uint32_t row_step = (uint32_t)C::RPI * K * 2u;  // bytes between instructions
+    const uint32_t row_w = (uint32_t)ii0 * row_step;
+    const bool gather_a = tw == 0 && gather != nullptr;
+    const int rl = lane / C::CPR, cl = lane % C::CPR;
+    int chunk[2];
+    uint32_t lane_off[2];
+#pragma unroll
+    for (int par = 0; par < 2; ++par) {
+      chunk[par] = cl ^ swz<C::CPR>(par * 8 + rl);
+      lane_off[par] = ((uint32_t)rl * K + chunk[par] * 8) * 2u;
+    }
+    auto par_of = [](int q) { return (q * C::RPI >> 3) & 1; };
+    // source byte offset of this lane's chunk in instruction q (K slab 0)
+    uint32_t off_q[NLD];
 #pragma unroll
     for (int q = 0; q < NLD; ++q) {
-      const bool is_a = q < C::A_PER;
-      const int jj = is_a ? q : q - C::A_PER;
-      const int tb = is_a ? 0 : 1 + jj / C::B_PER;
-      const int ii = wave * (is_a ? C::A_PER : C::B_PER) + (is_a ? jj : jj % C::B_PER);
-      const int r = ii * C::RPI + lane / C::CPR;
-      const int c = (lane % C::CPR) ^ swz<C::CPR>(r);
-      g_k[q] = c * 8;
-      l_dst[q] = __builtin_amdgcn_readfirstlane((tb == 0 ? 0 : C::A_BYTES + (tb - 1) * C::B_BYTES) +
-                                                ii * 1024);
-      if (is_a) {
-        if (gather == nullptr) {
-          g_off[q] = (uint32_t)(r * K + c * 8) * 2u;
-        } else {
-          const int s = (row0 + r < row_end) ? src_row(gather, kdiv, row0 + r, a_rows) : -1;
-          g_off[q] = s < 0 ? kOob : ((uint32_t)s * K + c * 8) * 2u;
-        }
+      if (gather_a) {
+        const int r = (ii0 + q) * C::RPI + rl;
+        const int s = (row0 + r < row_end) ? src_row(gather, kdiv, row0 + r, a_rows) : -1;
+        off_q[q] = s < 0 ? kOob : ((uint32_t)s * K + chunk[par_of(q)] * 8) * 2u;
       } else {
-        g_off[q] = (uint32_t)(r * K + c * 8) * 2u;
+        off_q[q] = row_w + (uint32_t)q * row_step + lane_off[par_of(q)];
       }
     }
     const uint32_t smem_base = lds_addr(smem);
-    // prefetch row of this thread: tile (wave-uniform) and byte offset of the row
-    const int pf_t = __builtin_amdgcn_readfirstlane(tid < BM ? 0 : 1 + (tid - BM) / BN);
-    uint32_t pf_off = kOob;
-    if constexpr (PF > 0) {
-      const int pr = tid < BM ? tid : (tid - BM) % BN;
-      if (pf_t > 0 || gather == nullptr) {
-        pf_off = (uint32_t)pr * K * 2u;
-      } else {
-        const int s = (row0 + pr < row_end) ? src_row(gather, kdiv, row0 + pr, a_rows) : -1;
-        pf_off = s < 0 ? kOob : (uint32_t)s * K * 2u;
-      }
-    }
-    const __amdgpu_buffer_rsrc_t rsrc_pf = make_rsrc_u(
-        pf_t == 0 ? t_base[0] : (pf_t == 1 ? t_base[1] : t_base[C::NB]),
-        pf_t == 0 ? t_bytes[0] : (pf_t == 1 ? t_bytes[1] : t_bytes[C::NB]));
-    const uint32_t junk = __builtin_amdgcn_readfirstlane(lds_addr(smem + NST * C::STAGE));
-    const int nk_real = (K + BK - 1) / BK;
-    auto prefetch = [&](int kt) {
-      const bool ok = pf_off != kOob && kt < nk_real;
-      dma16(rsrc_pf, ok ? pf_off + (uint32_t)kt * BK * 2u : kOob, junk);
-    };
-    // DMA instruction q of stage kt into LDS buffer buf (stages past K read zeros)
+    // DMA instruction q (of this issuing wave) of stage kt into LDS buffer
+    // buf; stages past K read zeros
+    const uint32_t lds_base = smem_base + lds_w;
     auto issue_one = [&](int kt, int buf, int q) {
-      const bool is_a = q < C::A_PER;
-      const __amdgpu_buffer_rsrc_t r = is_a ? rsrc[0] : rsrc[1 + (q - C::A_PER) / C::B_PER];
       const int k0 = kt * BK;
-      const uint32_t voff =
-          (k0 + g_k[q] < K && g_off[q] != kOob) ? g_off[q] + (uint32_t)k0 * 2u : kOob;
-      dma16(r, voff, smem_base + (uint32_t)buf * C::STAGE + l_dst[q]);
+      const bool ok = k0 + chunk[par_of(q)] * 8 < K && off_q[q] != kOob;
+      dma16(rsrc_w, ok ? off_q[q] + (uint32_t)k0 * 2u : kOob, lds_base, buf * C::STAGE + q * 1024);
     };
 
     f32x16 acc[C::NB][C::SM][C::SN];
@@ -599,12 +595,11 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
     constexpr int NR = C::SM + C::NB * C::SN;  // fragment reads per k16 step
     static_assert(NR <= NM, "one fragment read per MFMA");
     // One k16 step in a fixed order: MFMA t of fragment slot `slot`, then
-    // fragment read t of (rbuf, rks) into the other slot (rks >= 0), then the
-    // DMA instructions [q0, q1) of stage dkt (buffer dbuf) spread evenly over
-    // the MFMAs, and the prefetch of stage pkt (>= 0) after the last MFMA.  A
-    // burst of DMA instructions would stall the wave on the address queue
-    // while its MFMA pipe drains; spread out, the queue drains under the MFMAs.
-    auto kstep = [&](int slot, int rbuf, int rks, int dkt, int dbuf, int q0, int q1, int pkt) {
+    // fragment read t of (rbuf, rks) into the other slot (rks >= 0), then (in
+    // an issuing wave) the DMA instructions [q0, q1) of stage dkt (buffer
+    // dbuf) spread evenly over the MFMAs.
+    auto kstep = [&](auto producer, int slot, int rbuf, int rks, int dkt, int dbuf, int q0,
+                     int q1) {
       const unsigned char* sa = smem + rbuf * C::STAGE;
 #pragma unroll
       for (int t = 0; t < NM; ++t) {
@@ -621,10 +616,11 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
                 sa + b_row + xo[rks] + ub * C::B_BYTES + uj * 32 * C::RB);
           }
         }
+        if constexpr (decltype(producer)::value) {
 #pragma unroll
-        for (int q = q0; q < q1; ++q)
-          if ((q - q0) * NM / (q1 - q0) == t) issue_one(dkt, dbuf, q);
-        if (t == NM - 1 && pkt >= 0) prefetch(pkt);
+          for (int q = q0; q < q1; ++q)
+            if ((q - q0) * NM / (q1 - q0) == t) issue_one(dkt, dbuf, q);
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
     };
@@ -640,40 +636,40 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
     constexpr int DS = NST == 2 ? (KS - 2 > 1 ? KS - 2 : 1) : KS;
     constexpr int BEFORE = NST == 2 ? NLD : (KS - 1) * NLD / KS;
     // loads allowed in flight at the barrier of iteration kt (stage kt+1
-    // complete): the later stages' DMAs issued so far and the prefetch
-    constexpr int VM_AT_BARRIER =
-        NST == 2 ? (PF > 0 ? 1 : 0) : (NST - 3) * NLD + BEFORE;
+    // complete): the later stages' DMAs issued so far
+    constexpr int VM_AT_BARRIER = NST == 2 ? 0 : (NST - 3) * NLD + BEFORE;
     static_assert(VM_AT_BARRIER <= 63, "vmcnt range");
     auto qof = [&](int st) { return st >= DS ? NLD : st * NLD / DS; };
-    auto iteration = [&](int kt, int b) {
+    auto iteration = [&](auto producer, int kt, int b) {
       const int dkt = kt + NST - 1, dbuf = (b + NST - 1) % NST;
-      const int pkt = PF > 0 ? kt + 1 + PF : -1;
 #pragma unroll
       for (int st = 0; st + 1 < KS; ++st)
-        kstep(st & 1, b, st + 1, dkt, dbuf, qof(st), qof(st + 1),
-              st == (DS < KS - 1 ? DS : KS - 1) - 1 ? pkt : -1);
+        kstep(producer, st & 1, b, st + 1, dkt, dbuf, qof(st), qof(st + 1));
       vm_barrier<VM_AT_BARRIER>();
-      kstep((KS - 1) & 1, (b + 1) % NST, 0, dkt, dbuf, qof(KS - 1), qof(KS), -1);
+      kstep(producer, (KS - 1) & 1, (b + 1) % NST, 0, dkt, dbuf, qof(KS - 1), qof(KS));
     };
-
+    // the K loop, specialised for issuing and non-issuing waves (both meet
+    // the same barriers)
+    auto k_loop = [&](auto producer) {
+      if constexpr (decltype(producer)::value) {
 #pragma unroll
-    for (int st = 0; st < NST - 1; ++st)
+        for (int st = 0; st < NST - 1; ++st)
 #pragma unroll
-      for (int q = 0; q < NLD; ++q) issue_one(st, st, q);
-    if constexpr (PF > 0) {
-#pragma unroll
-      for (int st = 1; st <= PF; ++st) prefetch(st);
-      vm_barrier<PF>();
-    } else {
+          for (int q = 0; q < NLD; ++q) issue_one(st, st, q);
+      }
       vm_barrier<NLD * (NST - 2)>();
-    }
-    fload(0, 0, 0);
-    for (int kt = 0; kt < nk; kt += NST) {
+      fload(0, 0, 0);
+      for (int kt = 0; kt < nk; kt += NST) {
 #pragma unroll
-      for (int u = 0; u < NST; ++u) iteration(kt + u, u);
-    }
-    // the last DMAs (zeros past K) land before the buffers are reused
-    vm_barrier<0>();
+        for (int u = 0; u < NST; ++u) iteration(producer, kt + u, u);
+      }
+      // the last DMAs (zeros past K) land before the buffers are reused
+      vm_barrier<0>();
+    };
+    if (wave_u < C::NP)
+      k_loop(std::true_type{});
+    else
+      k_loop(std::false_type{});
 
     // epilogue: lane holds row m = .. + lane%32, columns n = .. + 8q + 4*(lane/32) + [0,4)
 #pragma unroll
@@ -929,7 +925,7 @@ int device_cus() {
   return n / 8 * 8;
 }
 
-template <int BM, int BN, int WM, int WN, int BK, int NST, int PF, int GM, int PERSIST, bool GATEUP>
+template <int BM, int BN, int WM, int WN, int BK, int NST, int PW, int GM, int PERSIST, bool GATEUP>
 void launch_gemm_dma(const bf16* A, const int32_t* gather, int kdiv, int a_rows,
                      const int32_t* offsets, int E, int rows, const bf16* B0, const bf16* B1,
                      int N, int K, bf16* out, hipStream_t s, const char* name) {
@@ -943,16 +939,16 @@ void launch_gemm_dma(const bf16* A, const int32_t* gather, int kdiv, int a_rows,
   }
   dim3 grid((unsigned)nb);
   ProfileScope ps(name, s);
-  hipLaunchKernelGGL((grouped_gemm_dma<BM, BN, WM, WN, GATEUP, BK, NST, PF, GM, PERSIST != 0>), grid,
+  hipLaunchKernelGGL((grouped_gemm_dma<BM, BN, WM, WN, GATEUP, BK, NST, PW, GM, PERSIST != 0>), grid,
                      dim3(WM * WN * kWave), 0, s, A, gather, kdiv, a_rows, offsets, E, rows, B0,
                      B1, N, K, out, ntn, (int)n_tiles);
 }
 
-template <int BM, int BN, int WM, int WN, int BK, int NST, int PF, int GM, int PERSIST>
+template <int BM, int BN, int WM, int WN, int BK, int NST, int PW, int GM, int PERSIST>
 struct DmaLaunch {
   template <bool GATEUP, typename... Args>
   static void run(Args... args) {
-    launch_gemm_dma<BM, BN, WM, WN, BK, NST, PF, GM, PERSIST, GATEUP>(args...);
+    launch_gemm_dma<BM, BN, WM, WN, BK, NST, PW, GM, PERSIST, GATEUP>(args...);
   }
 };
 
