@@ -36,7 +36,13 @@
 #define FOE_PIPE_OPT 1, 2
 #endif
 #ifndef FOE_SKINNY
-#define FOE_SKINNY 4, 4
+#define FOE_SKINNY 2, 1
+#endif
+#ifndef FOE_SKINNY_PIPE
+#define FOE_SKINNY_PIPE 0
+#endif
+#ifndef FOE_SKINNY_ROT
+#define FOE_SKINNY_ROT 1
 #endif
 // LDS-DMA large-M kernel: on/off; (BM, BN, WM, WN, BK, LDS stages, waves that
 // issue the DMA (0 = all), M-tile group of the tile order, persistent)
@@ -767,6 +773,7 @@ __global__ __launch_bounds__(KW * 64) void ffn_skinny_bf16(
   const uint32_t w_off1 = GATEUP ? w_off0 : (uint32_t)(r16 + 16) * K * 2u + kq * 2u;
   const __amdgpu_buffer_rsrc_t ar = make_rsrc(A, (uint32_t)a_rows * K * 2u);
   const int nchunks = (K + 31) / 32;
+  const int k_rot = (int)((blockIdx.x * 37u) % (unsigned)nchunks) / (KW * U) * (KW * U);
 
   for (int t0 = a; t0 < b; t0 += 32) {
     const int tv = min(32, b - t0);
@@ -782,18 +789,25 @@ __global__ __launch_bounds__(KW * 64) void ffn_skinny_bf16(
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int c0 = wave * U; c0 < nchunks; c0 += KW * U) {
-      u32x4 wa[U][2], xb[U][2];
+    // batches of U chunks, two register sets: the loads of the next batch are
+    // in flight while the MFMAs of the current one run
+    u32x4 wa[2][U][2], xb[2][U][2];
+    auto load = [&](int set, int c0) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int c = c0 + u;
+        int c = c0 + u;
+        // workgroups start their K walk at different chunks, so that at any
+        // moment they read different column ranges of their weight rows
+        if constexpr (FOE_SKINNY_ROT) c = c < nchunks ? (c + k_rot) % nchunks : c;
         const bool ok = c < nchunks && (uint32_t)c * 32u + kq < (uint32_t)K;
         const uint32_t kb = (uint32_t)c * 64u;
-        wa[u][0] = buf_load16_stream(wr0, ok ? w_off0 + kb : kOob);
-        wa[u][1] = buf_load16_stream(wr1, ok ? w_off1 + kb : kOob);
-        xb[u][0] = buf_load16(ar, (ok && a_off[0] != kOob) ? a_off[0] + kb : kOob);
-        xb[u][1] = buf_load16(ar, (ok && a_off[1] != kOob) ? a_off[1] + kb : kOob);
+        wa[set][u][0] = buf_load16_stream(wr0, ok ? w_off0 + kb : kOob);
+        wa[set][u][1] = buf_load16_stream(wr1, ok ? w_off1 + kb : kOob);
+        xb[set][u][0] = buf_load16(ar, (ok && a_off[0] != kOob) ? a_off[0] + kb : kOob);
+        xb[set][u][1] = buf_load16(ar, (ok && a_off[1] != kOob) ? a_off[1] + kb : kOob);
       }
+    };
+    auto compute = [&](int set) {
 #pragma unroll
       for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -801,8 +815,25 @@ __global__ __launch_bounds__(KW * 64) void ffn_skinny_bf16(
 #pragma unroll
           for (int j = 0; j < 2; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, wa[u][i]), __builtin_bit_cast(bf16x8, xb[u][j]),
+                __builtin_bit_cast(bf16x8, wa[set][u][i]), __builtin_bit_cast(bf16x8, xb[set][u][j]),
                 acc[i][j], 0, 0, 0);
+    };
+    constexpr int STEP = KW * U;
+    if constexpr (FOE_SKINNY_PIPE) {
+      int c0 = wave * U;
+      if (c0 < nchunks) load(0, c0);
+      for (; c0 < nchunks; c0 += 2 * STEP) {
+        if (c0 + STEP < nchunks) load(1, c0 + STEP);
+        compute(0);
+        if (c0 + STEP >= nchunks) break;
+        if (c0 + 2 * STEP < nchunks) load(0, c0 + 2 * STEP);
+        compute(1);
+      }
+    } else {
+      for (int c0 = wave * U; c0 < nchunks; c0 += STEP) {
+        load(0, c0);
+        compute(0);
+      }
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i)
