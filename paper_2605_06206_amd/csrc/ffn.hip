@@ -55,6 +55,25 @@
 #ifndef FOE_DMA_DN
 #define FOE_DMA_DN 256, 256, 2, 4, 64, 2, 4, 4, 1
 #endif
+// few rows per expert (decode): the same kernel on 32-row tiles whose loads
+// cover 4 weight rows x 256 bytes each (the fastest HBM pattern measured),
+// or (FOE_DECODE_DMA 0) the register-streaming kernel
+#ifndef FOE_DECODE_DMA
+#define FOE_DECODE_DMA 0
+#endif
+// few rows per expert: per-wave LDS-staged weight stream (stages in flight)
+#ifndef FOE_DECODE_STREAM
+#define FOE_DECODE_STREAM 1
+#endif
+#ifndef FOE_STREAM_NS
+#define FOE_STREAM_NS 3
+#endif
+#ifndef FOE_DMA_GU_DEC
+#define FOE_DMA_GU_DEC 32, 32, 1, 1, 128, 3, 1, 0, 0
+#endif
+#ifndef FOE_DMA_DN_DEC
+#define FOE_DMA_DN_DEC 32, 64, 1, 2, 128, 3, 1, 0, 0
+#endif
 
 namespace foe {
 namespace {
@@ -425,10 +444,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc_u(const void* base, 
 }
 // LDS destination = lds + imm; imm is a constant once the call is inlined
 // (the library is built with optimisation), so the per-instruction LDS
-// addresses cost no registers.
+// addresses cost no registers.  An LDS-DMA load that reads M0 needs one wait
+// state after the scalar write of M0 (the s_nop).
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds,
                                       int imm) {
-  asm volatile("s_add_u32 m0, %2, %3\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff),
+  asm volatile("s_add_u32 m0, %2, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff),
                "s"(r), "s"(lds), "i"(imm)
                : "memory");
 }
@@ -440,8 +460,9 @@ __device__ __forceinline__ void vm_barrier() {
 }
 template <int CPR>
 __device__ __forceinline__ int swz(int r) {
-  static_assert(CPR == 4 || CPR == 8, "rows of 64 or 128 bytes");
-  if constexpr (CPR == 8) return (r & 7) ^ ((r >> 3) & 1);
+  static_assert(CPR == 4 || CPR == 8 || CPR == 16, "rows of 64, 128 or 256 bytes");
+  if constexpr (CPR == 16) return r & 15;
+  else if constexpr (CPR == 8) return (r & 7) ^ ((r >> 3) & 1);
   else return ((r >> 1) & 3) ^ ((r >> 3) & 1);
 }
 
@@ -457,15 +478,19 @@ struct DmaCfg {
   static constexpr int RPI = 1024 / RB;    // rows per DMA instruction
   static constexpr int A_INS = BM / RPI, B_INS = BN / RPI;  // DMA instructions per tile
   static constexpr int NLD = (A_INS + NB * B_INS) / NP;      // per issuing wave
+  // the swizzle of a row depends on row & 15, so on instruction ii through
+  // ii & (NVAR - 1)
+  static constexpr int NVAR = RPI >= 16 ? 1 : 16 / RPI;
   static constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB;
   static constexpr int STAGE = A_BYTES + NB * B_BYTES;
   static constexpr int KS = BK / 16;       // k16 steps per stage
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be a multiple of 32");
   static_assert(BM % RPI == 0 && BN % RPI == 0 && (A_INS + NB * B_INS) % NP == 0 && NP <= NW,
                 "even DMA split");
-  // the instructions of an issuing wave stay inside one tile, and the row
-  // parity that selects the swizzle follows the instruction index
-  static_assert(A_INS % NLD == 0 && B_INS % NLD == 0 && (NLD * RPI / 8) % 2 == 0,
+  // with several issuing waves, the instructions of one wave stay inside one
+  // tile and start at a multiple of NVAR (a single issuing wave maps every
+  // instruction to its tile at compile time)
+  static_assert(NP == 1 || (A_INS % NLD == 0 && B_INS % NLD == 0 && NLD % NVAR == 0),
                 "one tile per issuing wave");
   static_assert(KS % 2 == 0, "fragment slots alternate within a stage");
   static_assert(NST >= 2 && NLD * (NST - 2) <= 63, "vmcnt range");
@@ -517,13 +542,31 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
       t_bytes[2] = t_bytes[1];
     }
 
-    // Issuing wave p loads instructions p*NLD .. p*NLD+NLD-1 of the stage (A
-    // tile first, then each weight tile; 1 KiB = RPI rows each), all inside
-    // tile tw starting at its instruction ii0.  Lane l lands in row rl = l/CPR,
-    // slot l%CPR of an instruction's rows and so fetches chunk
-    // (l%CPR) ^ swz(row); the swizzle depends on the instruction only through
-    // the parity of its first row / 8, so each lane keeps two chunk choices.
-    // Gathered A rows keep one source offset per instruction.
+    // DMA instruction gq of a stage covers RPI rows (1 KiB) of the A tile
+    // (gq < A_INS) or of a weight tile.  Lane l lands in row rl = l/CPR, slot
+    // l%CPR of the instruction's rows and so fetches chunk (l%CPR) ^ swz(row);
+    // the swizzle depends on the instruction only through its variant
+    // ii & (NVAR-1), so each lane keeps NVAR chunk choices.  Gathered A rows
+    // keep one source offset per A instruction.
+    const int rl = lane / C::CPR, cl = lane % C::CPR;
+    int chunk[C::NVAR];
+    uint32_t lane_off[C::NVAR];
+#pragma unroll
+    for (int v = 0; v < C::NVAR; ++v) {
+      chunk[v] = cl ^ swz<C::CPR>(v * C::RPI + rl);
+      lane_off[v] = ((uint32_t)rl * K + chunk[v] * 8) * 2u;
+    }
+    constexpr int NV = C::NVAR;
+    const uint32_t row_step = (uint32_t)C::RPI * K * 2u;  // bytes between instructions
+    auto a_src = [&](int ii) {  // gathered source offset of A instruction ii
+      const int r = ii * C::RPI + rl;
+      const int s = (row0 + r < row_end) ? src_row(gather, kdiv, row0 + r, a_rows) : -1;
+      return s < 0 ? kOob : ((uint32_t)s * K + chunk[ii & (NV - 1)] * 8) * 2u;
+    };
+    const uint32_t smem_base = lds_addr(smem);
+
+    // Several issuing waves: wave p loads instructions p*NLD .. p*NLD+NLD-1,
+    // all inside tile tw starting at its instruction ii0.
     const int p = min(wave_u, C::NP - 1);
     const int tw = p * NLD < C::A_INS ? 0 : 1 + (p * NLD - C::A_INS) / C::B_INS;
     const int ii0 = tw == 0 ? p * NLD : (p * NLD - C::A_INS) % C::B_INS;
@@ -531,38 +574,44 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
         make_rsrc_u(tw == 0 ? t_base[0] : (tw == 1 ? t_base[1] : t_base[C::NB]),
                     tw == 0 ? t_bytes[0] : (tw == 1 ? t_bytes[1] : t_bytes[C::NB]));
     const uint32_t lds_w = (tw == 0 ? 0 : C::A_BYTES + (tw - 1) * C::B_BYTES) + ii0 * 1024;
-    const uint32_t row_step = (uint32_t)C::RPI * K * 2u;  // bytes between instructions
-    const uint32_t row_w = (uint32_t)ii0 * row_step;
     const bool gather_a = tw == 0 && gather != nullptr;
-    const int rl = lane / C::CPR, cl = lane % C::CPR;
-    int chunk[2];
-    uint32_t lane_off[2];
-#pragma unroll
-    for (int par = 0; par < 2; ++par) {
-      chunk[par] = cl ^ swz<C::CPR>(par * 8 + rl);
-      lane_off[par] = ((uint32_t)rl * K + chunk[par] * 8) * 2u;
-    }
-    auto par_of = [](int q) { return (q * C::RPI >> 3) & 1; };
     // source byte offset of this lane's chunk in instruction q (K slab 0)
-    uint32_t off_q[NLD];
+    uint32_t off_q[C::NP > 1 ? NLD : 1];
+    if constexpr (C::NP > 1) {
 #pragma unroll
-    for (int q = 0; q < NLD; ++q) {
-      if (gather_a) {
-        const int r = (ii0 + q) * C::RPI + rl;
-        const int s = (row0 + r < row_end) ? src_row(gather, kdiv, row0 + r, a_rows) : -1;
-        off_q[q] = s < 0 ? kOob : ((uint32_t)s * K + chunk[par_of(q)] * 8) * 2u;
-      } else {
-        off_q[q] = row_w + (uint32_t)q * row_step + lane_off[par_of(q)];
-      }
+      for (int q = 0; q < NLD; ++q)
+        off_q[q] = gather_a ? a_src(ii0 + q)
+                            : (uint32_t)(ii0 + q) * row_step + lane_off[q & (NV - 1)];
     }
-    const uint32_t smem_base = lds_addr(smem);
+    // A single issuing wave: instruction q is fixed at compile time.
+    __amdgpu_buffer_rsrc_t rsrc_t[1 + C::NB];
+    uint32_t a_off[C::NP == 1 ? C::A_INS : 1];
+    if constexpr (C::NP == 1) {
+#pragma unroll
+      for (int t = 0; t <= C::NB; ++t) rsrc_t[t] = make_rsrc_u(t_base[t], t_bytes[t]);
+#pragma unroll
+      for (int ii = 0; ii < C::A_INS; ++ii)
+        a_off[ii] = gather != nullptr ? a_src(ii) : (uint32_t)ii * row_step + lane_off[ii & (NV - 1)];
+    }
+
     // DMA instruction q (of this issuing wave) of stage kt into LDS buffer
     // buf; stages past K read zeros
     const uint32_t lds_base = smem_base + lds_w;
     auto issue_one = [&](int kt, int buf, int q) {
       const int k0 = kt * BK;
-      const bool ok = k0 + chunk[par_of(q)] * 8 < K && off_q[q] != kOob;
-      dma16(rsrc_w, ok ? off_q[q] + (uint32_t)k0 * 2u : kOob, lds_base, buf * C::STAGE + q * 1024);
+      if constexpr (C::NP == 1) {
+        const int tb = q < C::A_INS ? 0 : 1 + (q - C::A_INS) / C::B_INS;
+        const int ii = q < C::A_INS ? q : (q - C::A_INS) % C::B_INS;
+        const uint32_t off =
+            tb == 0 ? a_off[ii] : (uint32_t)ii * row_step + lane_off[ii & (NV - 1)];
+        const bool ok = k0 + chunk[ii & (NV - 1)] * 8 < K && off != kOob;
+        dma16(rsrc_t[tb], ok ? off + (uint32_t)k0 * 2u : kOob, smem_base,
+              buf * C::STAGE + (tb == 0 ? 0 : C::A_BYTES + (tb - 1) * C::B_BYTES) + ii * 1024);
+      } else {
+        const bool ok = k0 + chunk[q & (NV - 1)] * 8 < K && off_q[q] != kOob;
+        dma16(rsrc_w, ok ? off_q[q] + (uint32_t)k0 * 2u : kOob, lds_base,
+              buf * C::STAGE + q * 1024);
+      }
     };
 
     f32x16 acc[C::NB][C::SM][C::SN];
@@ -599,7 +648,7 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
     };
     constexpr int NM = C::NB * C::SM * C::SN;  // MFMAs per k16 step
     constexpr int NR = C::SM + C::NB * C::SN;  // fragment reads per k16 step
-    static_assert(NR <= NM, "one fragment read per MFMA");
+    constexpr int NT = NM > NR ? NM : NR;  // slots of a k16 step
     // One k16 step in a fixed order: MFMA t of fragment slot `slot`, then
     // fragment read t of (rbuf, rks) into the other slot (rks >= 0), then (in
     // an issuing wave) the DMA instructions [q0, q1) of stage dkt (buffer
@@ -608,10 +657,12 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
                      int q1) {
       const unsigned char* sa = smem + rbuf * C::STAGE;
 #pragma unroll
-      for (int t = 0; t < NM; ++t) {
-        const int b = t / (C::SN * C::SM), j = (t / C::SM) % C::SN, i = t % C::SM;
-        acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[slot][b][j], xa[slot][i],
-                                                               acc[b][i][j], 0, 0, 0);
+      for (int t = 0; t < NT; ++t) {
+        if (t < NM) {
+          const int b = t / (C::SN * C::SM), j = (t / C::SM) % C::SN, i = t % C::SM;
+          acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[slot][b][j], xa[slot][i],
+                                                                 acc[b][i][j], 0, 0, 0);
+        }
         if (rks >= 0 && t < NR) {
           if (t < C::SM) {
             xa[slot ^ 1][t] =
@@ -625,7 +676,7 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
         if constexpr (decltype(producer)::value) {
 #pragma unroll
           for (int q = q0; q < q1; ++q)
-            if ((q - q0) * NM / (q1 - q0) == t) issue_one(dkt, dbuf, q);
+            if ((q - q0) * NT / (q1 - q0) == t) issue_one(dkt, dbuf, q);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -880,6 +931,169 @@ __global__ __launch_bounds__(KW * 64) void ffn_skinny_bf16(
   }
 }
 
+// Few rows per expert (decode), LDS-staged weight stream.  A workgroup of 4
+// waves takes one expert and 4 consecutive weight tiles (each 16 gate + 16 up
+// rows, or 32 down rows), one per wave, over all of K, for up to 32 rows of A
+// (tokens) at a time.  Operands stream through a ring of NS LDS stages of
+// 128 K columns: per stage each wave loads its weight tile with 8 LDS-DMA
+// instructions and a quarter of the shared token tile with 2, each
+// instruction covering 4 rows x 256 bytes (the access pattern that reads HBM
+// fastest).  The 16-byte chunk c of row r of any tile sits in slot
+// c ^ (r & 15), so the v_mfma_f32_16x16x32_bf16 fragment reads (16 rows, one
+// chunk) are conflict-free.
+//
+// All loads of the loop are LDS DMA issued from inline assembly with explicit
+// vmcnt waits, so NS-2 later stages stay in flight while a stage is used.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <bool GATEUP, int NS>
+__global__ __launch_bounds__(256) void ffn_stream_bf16(
+    const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv, int a_rows,
+    const int32_t* __restrict__ offsets, int E, int rows, const bf16* __restrict__ W0,
+    const bf16* __restrict__ W1, int N, int K, bf16* __restrict__ out, int n_groups) {
+  static_assert(NS >= 2 && NS <= 4, "2 to 4 stages");
+  constexpr int WPB = 4;
+  constexpr int NPW = GATEUP ? 16 : 32;  // output columns per wave
+  constexpr int WB = 8192;                // weight bytes per stage and wave
+  constexpr int XB = WPB * WB;            // offset of the token rows in a stage
+  constexpr int SB = XB + 8192;           // bytes per stage
+  constexpr int NI = 10;                  // DMA instructions per stage and wave
+  static_assert(NS * SB <= 160 * 1024, "LDS capacity");
+  __shared__ __align__(1024) unsigned char smem[NS * SB];
+
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  const int gpe = (n_groups + WPB - 1) / WPB;                           // workgroups per expert
+  const int e = blockIdx.x / gpe;
+  if (e >= E) return;
+  const int n0 = ((blockIdx.x % gpe) * WPB + wave) * NPW;
+  const int a = min(max(offsets[e], 0), rows);
+  const int b = max(min(max(offsets[e + 1], 0), rows), a);
+  if (b == a) return;  // uniform over the workgroup
+  const uint32_t lds0 = lds_addr(smem);
+
+  // weight sources: instruction i < 4 reads tile rows 4i.. of W0, i >= 4 rows
+  // 4(i-4).. of W1 (gate/up) or rows 4i.. of W0 (down); a wave past N reads
+  // zeros (empty range)
+  const int nv = max(min(NPW, N - n0), 0);
+  const size_t wrow = (size_t)e * N + min(n0, N);
+  const __amdgpu_buffer_rsrc_t wr0 = make_rsrc_u(W0 + wrow * K, (uint32_t)nv * K * 2u);
+  const __amdgpu_buffer_rsrc_t wr1 =
+      GATEUP ? make_rsrc_u(W1 + wrow * K, (uint32_t)nv * K * 2u) : wr0;
+  const __amdgpu_buffer_rsrc_t ar = make_rsrc_u(A, (uint32_t)a_rows * K * 2u);
+  const int lr = lane >> 4, lc = lane & 15;
+  uint32_t wv[8];  // byte offset of this lane's weight chunk in instruction i (stage 0)
+  int wk[8];       // its K column
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int tr = (GATEUP ? (i & 3) : i) * 4 + lr;  // row inside the rsrc range
+    const int q = lc ^ (tr & 15);                     // chunk of the 256-byte segment
+    wk[i] = q * 8;
+    wv[i] = ((uint32_t)tr * K + q * 8) * 2u;
+  }
+  const int nks = (K + 127) / 128;
+  // fragment read offsets inside a stage: row R of a 16-row tile
+  const int R = lane & 15, g = lane >> 4;
+  const int rbase = (R >> 2) * 1024 + (R & 3) * 256;
+
+  for (int t0 = a; t0 < b; t0 += 32) {
+    const int tv = min(32, b - t0);
+    // token instructions 2*wave and 2*wave+1 of this wave (rows 4i.. of the pass)
+    uint32_t xv[2];
+    int xk[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int t = (2 * wave + u) * 4 + lr;
+      const int q = lc ^ (t & 15);
+      const int sr = t < tv ? src_row(gather, kdiv, t0 + t, a_rows) : -1;
+      xk[u] = q * 8;
+      xv[u] = sr < 0 ? kOob : ((uint32_t)sr * K + q * 8) * 2u;
+    }
+    auto issue = [&](int kt, int s) {
+      const int k0 = kt * 128;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t off = k0 + wk[i] < K ? wv[i] + (uint32_t)k0 * 2u : kOob;
+        dma16(GATEUP && i >= 4 ? wr1 : wr0, off, lds0 + wave * WB, s * SB + i * 1024);
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const uint32_t off = (k0 + xk[u] < K && xv[u] != kOob) ? xv[u] + (uint32_t)k0 * 2u : kOob;
+        dma16(ar, off, lds0 + wave * 2048, s * SB + XB + u * 1024);
+      }
+    };
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // iteration kt: wait for this wave's part of stage kt, meet the other
+    // waves (stage kt complete, stage kt-1 no longer read), issue stage
+    // kt+NS-1 into the buffer of stage kt-1, use stage kt
+    auto body = [&](int kt, int s, int s_next) {
+      if (kt + NS - 2 < nks) vm_wait<NI * (NS - 2)>();
+      else vm_wait<0>();
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      if (kt + NS - 1 < nks) issue(kt + NS - 1, s_next);
+      const unsigned char* src = smem + s * SB + rbase;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int slot = ((c * 4 + g) ^ R) * 16;
+        const bf16x8 w0 = *reinterpret_cast<const bf16x8*>(src + wave * WB + slot);
+        const bf16x8 w1 = *reinterpret_cast<const bf16x8*>(src + wave * WB + 4096 + slot);
+        const bf16x8 x0 = *reinterpret_cast<const bf16x8*>(src + XB + slot);
+        const bf16x8 x1 = *reinterpret_cast<const bf16x8*>(src + XB + 4096 + slot);
+        acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, x0, acc[0][0], 0, 0, 0);
+        acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, x0, acc[1][0], 0, 0, 0);
+        acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, x1, acc[0][1], 0, 0, 0);
+        acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, x1, acc[1][1], 0, 0, 0);
+      }
+    };
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+      if (s < nks) issue(s, s);
+    for (int kt0 = 0; kt0 < nks; kt0 += NS) {
+#pragma unroll
+      for (int u = 0; u < NS; ++u) {
+        const int kt = kt0 + u;
+        if (kt < nks) body(kt, u, (u + NS - 1) % NS);
+      }
+    }
+    // every wave is done with the ring before the next pass refills it
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+    // lane holds weight rows 4*(lane/16) + [0,4) of each tile for token lane%16 (+16)
+    const int nb = 4 * g;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int t = j * 16 + R;
+      if (t >= tv) continue;
+      bf16* orow = out + (size_t)(t0 + t) * N + n0;
+      if constexpr (GATEUP) {
+        if (nb < nv) {
+          bf16x4 o;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) o[v] = (bf16)(silu_f(acc[0][j][v]) * acc[1][j][v]);
+          *reinterpret_cast<bf16x4*>(orow + nb) = o;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          if (i * 16 + nb >= nv) continue;
+          bf16x4 o;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) o[v] = (bf16)acc[i][j][v];
+          *reinterpret_cast<bf16x4*>(orow + i * 16 + nb) = o;
+        }
+      }
+    }
+  }
+}
+
 constexpr int kSkinnyWaves = FirstOf<FOE_SKINNY>::value;
 
 // ---- fp32 path: plain FMA kernels (small shapes) ---------------------------
@@ -1017,7 +1231,28 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
   const bf16* wd = reinterpret_cast<const bf16*>(w_down);
   bf16* h = reinterpret_cast<bf16*>(scratch);
   bf16* y = reinterpret_cast<bf16*>(y_perm);
-  if (rows < 64 * E) {  // few rows per expert: weight-streaming bound
+  if (rows < 64 * E && FOE_DECODE_STREAM) {  // few rows per expert: weight-streaming bound
+    {
+      const int ng = ceil_div(F, 16);
+      ProfileScope ps("ffn_gateup", s);
+      hipLaunchKernelGGL((ffn_stream_bf16<true, FOE_STREAM_NS>), dim3(E * ceil_div(ng, 4)),
+                         dim3(256), 0, s, xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F,
+                         d, h, ng);
+    }
+    {
+      const int ng = ceil_div(d, 32);
+      ProfileScope ps("ffn_down", s);
+      hipLaunchKernelGGL((ffn_stream_bf16<false, FOE_STREAM_NS>), dim3(E * ceil_div(ng, 4)),
+                         dim3(256), 0, s, static_cast<const bf16*>(h), nullptr, 1, rows, offsets,
+                         E, rows, wd, nullptr, d, F, y, ng);
+    }
+  } else if (rows < 64 * E && FOE_DECODE_DMA) {
+    DmaLaunch<FOE_DMA_GU_DEC>::run<true>(xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F, d,
+                                         h, s, "ffn_gateup");
+    DmaLaunch<FOE_DMA_DN_DEC>::run<false>(static_cast<const bf16*>(h), (const int32_t*)nullptr, 1,
+                                          rows, offsets, E, rows, wd, (const bf16*)nullptr, d, F,
+                                          y, s, "ffn_down");
+  } else if (rows < 64 * E) {
     {
       const int ng = ceil_div(F, 16);
       ProfileScope ps("ffn_gateup", s);
