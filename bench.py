@@ -18,8 +18,9 @@ profiles/traffic.json; it is null when no measurement exists for this
 workload or the kernel's source has changed since it was taken.
 
 Timed passes (both over K steps, HIP events on the library's stream):
-  A  plain steps -> value / ms_per_step (replayed from HIP graphs unless
-     --no-graph; the eager time is reported beside it)
+  A  plain steps, launched eagerly and (unless --no-graph) replayed from HIP
+     graphs -> value / ms_per_step from the faster of the two (both times
+     are reported; config.launch names the one used)
   B  the same steps with every kernel bracketed by HIP events (the library's
      timing hooks) -> per-kernel average duration and the roofline object
 """
@@ -279,7 +280,9 @@ def main():
         for i in range(args.warmup):
             graphs[i % nsets].replay()
         graph_ms = timed(args.steps, lambda i: graphs[i % nsets].replay()) / args.steps
-    ms = graph_ms if graph_ms is not None else eager_ms
+    # both launch modes time the same steps; the faster one is the throughput
+    use_graph = graph_ms is not None and graph_ms < eager_ms
+    ms = graph_ms if use_graph else eager_ms
 
     # pass B: per-kernel HIP events (eager launches on the same stream)
     foe.profile_reset()
@@ -316,7 +319,7 @@ def main():
                 f"{nsets} rotated input/weight sets)",
         "config": {"workload": f"{args.config}: C={C} T={T} d={d} E={E} k={k} F={F} {dt}",
                    "C": C, "T": T, "d": d, "E": E, "k": k, "F": F,
-                   "launch": "hip_graph_replay" if graph_ms is not None else "eager"},
+                   "launch": "hip_graph_replay" if use_graph else "eager"},
         "block_tflops": round(flops / (ms * 1e-3) / 1e12, 3),
         "expert_ffn_tflops": round(6.0 * C * T * k * d * F / (ffn_ms * 1e-3) / 1e12, 3),
         "eager_ms_per_step": round(eager_ms, 6),
