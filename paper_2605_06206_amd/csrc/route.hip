@@ -9,7 +9,7 @@
 // MFMA result layout each row of 16 lanes holds all 16 experts of one token
 // (per accumulator register), so the top-k is k rounds of a (score desc, id
 // asc) arg-max across a 16-lane row with DPP rotations.
-#include "foe_common.hpp"
+#include "lds_dma.hpp"
 
 namespace foe {
 namespace {
@@ -214,6 +214,145 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
   }
 }
 
+// Many tokens, bf16, E <= 32: a workgroup of WPB waves takes 16 tokens per
+// wave over all of K, so no partial scores are exchanged.  x and W_r stream
+// through a ring of NS LDS stages of 128 K columns with LDS-DMA loads of 4
+// rows x 256 bytes (each wave loads its own token rows and a share of the
+// router rows), the 16-byte chunk c of row r stored in slot c ^ (r & 15).
+// Each wave then selects the top-k of its tokens from its own accumulators.
+template <int NT, int NS, int WPB>
+__global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
+    const bf16* __restrict__ x, const bf16* __restrict__ w, const float* __restrict__ bias,
+    int T_, int d, int E, int k, int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
+  constexpr int XB = WPB * 4096;          // token rows of a stage (16 rows x 256 B per wave)
+  constexpr int SB = XB + NT * 4096;      // + router rows (16 rows x 256 B per expert tile)
+  constexpr int WI = NT * 4 / WPB;        // router instructions per wave and stage
+  constexpr int NI = 4 + WI;              // DMA instructions per wave and stage
+  static_assert(NT * 4 % WPB == 0, "even split of the router rows");
+  static_assert(NS * SB + WPB * 8 * 32 * 4 <= 160 * 1024, "LDS capacity");
+  __shared__ __align__(1024) unsigned char smem[NS * SB];
+  __shared__ int sel_buf[WPB][8 * 32];
+
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int t0 = (blockIdx.x * WPB + wave) * 16;  // this wave's tokens
+  const uint32_t lds0 = lds_addr(smem);
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc_u(x, (uint32_t)T_ * d * 2u);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc_u(w, (uint32_t)E * d * 2u);
+  const int lr = lane >> 4, lc = lane & 15;
+  // token instruction i (rows t0+4i..) and router instruction wave*WI + j
+  uint32_t xv[4], wv[WI];
+  int xk[4], wk[WI];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 4 * i + lr;  // row in the 16-token tile
+    const int q = lc ^ (r & 15);
+    xk[i] = q * 8;
+    xv[i] = t0 + r < T_ ? ((uint32_t)(t0 + r) * d + q * 8) * 2u : kOob;
+  }
+#pragma unroll
+  for (int j = 0; j < WI; ++j) {
+    const int e = 4 * (wave * WI + j) + lr;  // router row
+    const int q = lc ^ (e & 15);
+    wk[j] = q * 8;
+    wv[j] = e < E ? ((uint32_t)e * d + q * 8) * 2u : kOob;
+  }
+  const int nks = (d + 127) / 128;
+  auto issue = [&](int kt, int s) {
+    const int k0 = kt * 128;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t off = (k0 + xk[i] < d && xv[i] != kOob) ? xv[i] + (uint32_t)k0 * 2u : kOob;
+      dma16(xr, off, lds0 + wave * 4096, s * SB + i * 1024);
+    }
+#pragma unroll
+    for (int j = 0; j < WI; ++j) {
+      const uint32_t off = (k0 + wk[j] < d && wv[j] != kOob) ? wv[j] + (uint32_t)k0 * 2u : kOob;
+      dma16(wr, off, lds0 + wave * WI * 1024, s * SB + XB + j * 1024);
+    }
+  };
+  const int R = lane & 15, g = lane >> 4;
+  const int rbase = (R >> 2) * 1024 + (R & 3) * 256;
+  f32x4 acc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto body = [&](int kt, int s, int s_next) {
+    if (kt + NS - 2 < nks) vm_wait<NI * (NS - 2)>();
+    else vm_wait<0>();
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (kt + NS - 1 < nks) issue(kt + NS - 1, s_next);
+    const unsigned char* src = smem + s * SB + rbase;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int slot = ((c * 4 + g) ^ R) * 16;
+      const bf16x8 xa = *reinterpret_cast<const bf16x8*>(src + wave * 4096 + slot);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const bf16x8 wb = *reinterpret_cast<const bf16x8*>(src + XB + nt * 4096 + slot);
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa, wb, acc[nt], 0, 0, 0);
+      }
+    }
+  };
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nks) issue(s, s);
+  for (int kt0 = 0; kt0 < nks; kt0 += NS) {
+#pragma unroll
+    for (int u = 0; u < NS; ++u) {
+      const int kt = kt0 + u;
+      if (kt < nks) body(kt, u, (u + NS - 1) % NS);
+    }
+  }
+
+  // accumulator register i holds token t0 + 4*(lane/16) + i (one per 16-lane
+  // row) and experts nt*16 + lane%16
+  const int col = lane & 15, row = lane >> 4;
+  int* sel_e = sel_buf[wave];
+  float* sel_v = reinterpret_cast<float*>(sel_e + 4 * k);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float gl[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int e = nt * 16 + col;
+      gl[nt] = acc[nt][i] + ((bias != nullptr && e < E) ? bias[e] : 0.f);
+    }
+    const int tok = t0 + 4 * row + i;
+    unsigned taken = 0;  // bit nt: expert nt*16 + col already selected / absent
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      if (nt * 16 + col >= E) taken |= 1u << nt;
+    for (int s = 0; s < k; ++s) {
+      float bv = -__builtin_inff();
+      int be = 0x7fffffff;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int e = nt * 16 + col;
+        if (!((taken >> nt) & 1u) && beats(gl[nt], e, bv, be)) { bv = gl[nt]; be = e; }
+      }
+      argmax_step<8>(bv, be);
+      argmax_step<4>(bv, be);
+      argmax_step<2>(bv, be);
+      argmax_step<1>(bv, be);
+      if (be != 0x7fffffff && (be & 15) == col) taken |= 1u << (be >> 4);
+      if (col == 0) {
+        sel_e[row * k + s] = (be == 0x7fffffff) ? -1 : be;
+        sel_v[row * k + s] = bv;
+      }
+    }
+    if (tok < T_) {
+      const float m = sel_v[row * k];
+      float z = 0.f;
+      for (int s = 0; s < k; ++s) z += expf(sel_v[row * k + s] - m);
+      const float inv = 1.0f / z;
+      for (int s = col; s < k; s += 16) {
+        topk_idx[(size_t)tok * k + s] = sel_e[row * k + s];
+        topk_w[(size_t)tok * k + s] = expf(sel_v[row * k + s] - m) * inv;
+      }
+    }
+  }
+}
+
 template <typename T, int NT, int NW, int TG>
 hipError_t launch_nt(int T_, int d, int E, int k, const void* x, const void* w,
                      const float* bias, int32_t* idx, float* wt, hipStream_t s) {
@@ -235,16 +374,50 @@ hipError_t launch_nt(int T_, int d, int E, int k, const void* x, const void* w,
 template <int TG_, int NW_> struct RouteCfg {
   static constexpr int TG = TG_, NW = NW_;
 };
+#ifndef FOE_ROUTE_STREAM
+#define FOE_ROUTE_STREAM 1
+#endif
+#ifndef FOE_ROUTE_STREAM_MIN_T
+#define FOE_ROUTE_STREAM_MIN_T 8192
+#endif
 #ifndef FOE_ROUTE_TG16
 #define FOE_ROUTE_TG16 1, 8
 #endif
 #ifndef FOE_ROUTE_TG32
 #define FOE_ROUTE_TG32 2, 8
 #endif
+template <int WPB>
+hipError_t launch_stream(int T_, int d, int E, int k, const void* x, const void* w,
+                         const float* bias, int32_t* idx, float* wt, hipStream_t s) {
+  constexpr int NS = 4;
+  dim3 grid(ceil_div(T_, 16 * WPB));
+  const bf16* xb = reinterpret_cast<const bf16*>(x);
+  const bf16* wb = reinterpret_cast<const bf16*>(w);
+  if (E <= 16)
+    hipLaunchKernelGGL((route_stream_kernel<1, NS, WPB>), grid, dim3(WPB * kWave), 0, s, xb, wb,
+                       bias, T_, d, E, k, idx, wt);
+  else
+    hipLaunchKernelGGL((route_stream_kernel<2, NS, WPB>), grid, dim3(WPB * kWave), 0, s, xb, wb,
+                       bias, T_, d, E, k, idx, wt);
+  return hipGetLastError();
+}
+
 template <typename T>
 hipError_t launch_t(int T_, int d, int E, int k, const void* x, const void* w, const float* bias,
                     int32_t* idx, float* wt, hipStream_t s) {
   const bool many = T_ >= 2048;
+  if constexpr (sizeof(T) == 2) {
+    // buffer offsets are 32-bit: x must span less than 2 GiB
+    if (FOE_ROUTE_STREAM && T_ >= FOE_ROUTE_STREAM_MIN_T && E <= 32 &&
+        (size_t)T_ * d * 2 < ((size_t)1 << 31)) {
+      // more waves per workgroup share each router row once there are enough
+      // tokens for every CU
+      ProfileScope ps("route", s);
+      if (T_ >= 16384)
+        return launch_stream<4>(T_, d, E, k, x, w, bias, idx, wt, s);
+      return launch_stream<2>(T_, d, E, k, x, w, bias, idx, wt, s);
+    }
+  }
   if (E <= 16)
     return many ? launch_nt<T, 1, RouteCfg<FOE_ROUTE_TG16>::NW, RouteCfg<FOE_ROUTE_TG16>::TG>(
                       T_, d, E, k, x, w, bias, idx, wt, s)

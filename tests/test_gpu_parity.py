@@ -124,6 +124,8 @@ def test_route_parity_configs(name):
     (1, 64, 4, 1, "bf16"), (50, 136, 5, 3, "bf16"), (333, 64, 33, 5, "bf16"),
     (77, 256, 256, 8, "bf16"), (40, 32, 16, 16, "f32"), (129, 8, 2, 2, "f32"),
     (300, 512, 64, 64, "bf16"),
+    # many-token streaming path: ragged token tails, K tail, partial expert tile
+    (8195, 136, 20, 3, "bf16"), (16389, 520, 32, 4, "bf16"), (9000, 264, 9, 2, "bf16"),
 ])
 def test_route_parity_shapes(T, d, E, k, dt):
     """Ragged token tails, K tails (d not a multiple of 32), E not a multiple
