@@ -95,7 +95,7 @@ BlockWs block_ws(foe_dtype dt, int C, int T, int d, int E, int k, int F) {
   take(w.sorted_src, CR * 4);
   take(w.row_of, CR * 4);
   take(w.y, CR * d * s);
-  take(w.perm, permute_scratch_bytes(T, k, E));
+  take(w.perm, permute_scratch_bytes(T, k, E, C));
   take(w.ffn, ffn_scratch_bytes(dt, (int)CR, F));
   w.total = align_up(off, 256);
   return w;
@@ -163,7 +163,7 @@ size_t foe_workspace_bytes(const char* op, foe_dtype dt, int C, int T, int d, in
   if (o == "permute") {
     check_route_shape(c, T, E, k);
     if (!c.err.empty()) return (g_err = c.err, SIZE_MAX);
-    return permute_scratch_bytes(T, k, E);
+    return permute_scratch_bytes(T, k, E, 1);
   }
   if (o == "expert_ffn") {
     c.need(T >= 0 && k >= 1 && (long long)T * k <= INT_MAX, "rows = T*k must be in [0, 2^31)");
@@ -219,7 +219,7 @@ int foe_permute(foe_dtype dt, int T, int d, int E, int k, const int32_t* topk_id
   c.small(row_of, any, "row_of");
   c.tensor(x_perm, any, "x_perm");
   if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_permute: " + c.err);
-  const size_t need = permute_scratch_bytes(T, k, E);
+  const size_t need = permute_scratch_bytes(T, k, E, 1);
   if (need > 0 && (ws == nullptr || !aligned16(ws)))
     return fail(FOE_ERR_INVALID, "foe_permute: ws is NULL or not 16-byte aligned");
   if (ws_bytes < need)

@@ -80,9 +80,9 @@ hipError_t launch_route(foe_dtype dt, int T, int d, int E, int k, const void* x,
                         const void* w_router, const float* bias, int32_t* topk_idx,
                         float* topk_w, hipStream_t s);
 
-// permute scratch = 2 * nblk * E int32 (see permute_blocks())
+// permute scratch = 2 * C * nblk * E int32 (see permute_blocks())
 int permute_blocks(int R);
-size_t permute_scratch_bytes(int T, int k, int E);
+size_t permute_scratch_bytes(int T, int k, int E, int C);
 // histogram / scan / stable ranks of C clusters' ids (topk_idx [C,T,k]);
 // offsets [C*E+1] and row_of values are global rows (cluster h starts at h*T*k)
 hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int32_t* counts,

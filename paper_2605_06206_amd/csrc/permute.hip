@@ -3,27 +3,79 @@
 //
 //   hist    : per-block expert counts of a chunk of kChunk pairs (LDS atomics;
 //             integer adds commute, so the counts are deterministic)
-//   scan    : one workgroup; per expert the exclusive prefix over blocks, then
-//             the exclusive prefix over experts -> offsets, block bases
-//   rank    : each block re-walks its chunk in flat order; a wave-level
-//             ballot/popcount gives each pair its rank among the earlier pairs
-//             of the same expert, so the order is (expert asc, flat index asc)
-//             whatever the atomics did
+//   rank    : one pair per thread.  A wave finds the lanes that share its
+//             lane's expert with ceil(log2 E) ballots (one per bit of the
+//             expert id), so a pair's rank among the earlier pairs of its
+//             expert in the wave is a popcount.  Per-wave counts, the counts
+//             of the earlier blocks and the per-expert totals give the base,
+//             and the order is (expert asc, flat index asc) whatever the
+//             atomics did.  The block counts are summed by every block, so
+//             there is no separate scan launch; past kFoldMax block counts a
+//             scan kernel writes the block bases instead.
 //   scatter : every token row of x is read once and written to its k
 //             destination rows with 128-bit stores
+// All clusters of a block run in one grid (blockIdx.y = cluster).
 #include "foe_common.hpp"
 
 namespace foe {
 namespace {
 
-constexpr int kChunk = 1024;            // pairs per block
-constexpr int kWavesP = 4;
-constexpr int kPerWave = kChunk / kWavesP;  // 512 pairs per wave
+constexpr int kChunk = 1024;  // pairs per block, one per thread in rank
+constexpr int kRankWaves = kChunk / kWave;
 constexpr int kMaxE = 256;
+constexpr int kFoldMax = 16384;  // block counts per cluster summed inside rank
 
-__global__ __launch_bounds__(256) void hist_kernel(const int32_t* __restrict__ idx, int R, int E,
-                                                   int32_t* __restrict__ block_counts) {
+// Lanes of the wave whose expert equals this lane's, among the lanes with ok:
+// the AND over the id's bits of the ballot of that bit or of its complement.
+// Valid when every expert id is below 2^nbits.
+__device__ __forceinline__ uint64_t match_expert(int e, bool ok, int nbits) {
+  uint64_t m = __ballot(ok);
+  for (int b = 0; b < nbits; ++b) {
+    const bool bit = (e >> b) & 1;
+    const uint64_t bb = __ballot(ok && bit);
+    m &= bit ? bb : ~bb;
+  }
+  return m;
+}
+
+__device__ __forceinline__ uint64_t lanes_below() {
+  const int lane = lane_id();
+  return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+}
+
+// Exclusive prefix of total[0..E) in place, total[E] = the sum; run by one
+// whole wave (E <= 256: four experts per lane).
+__device__ __forceinline__ void wave_excl_scan_experts(int* total, int E) {
+  const int lane = lane_id();
+  int v[4];
+  int sum = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = lane * 4 + j;
+    v[j] = i < E ? total[i] : 0;
+    sum += v[j];
+  }
+  int incl = sum;
+#pragma unroll
+  for (int dlt = 1; dlt < kWave; dlt <<= 1) {
+    const int t = __shfl_up(incl, dlt);
+    if (lane >= dlt) incl += t;
+  }
+  int run = incl - sum;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = lane * 4 + j;
+    if (i < E) total[i] = run;
+    run += v[j];
+  }
+  if (lane == kWave - 1) total[E] = incl;
+}
+
+__global__ __launch_bounds__(256) void hist_kernel(const int32_t* __restrict__ idx_all, int R,
+                                                   int E, int32_t* __restrict__ block_counts_all) {
   __shared__ int cnt[kMaxE];
+  const int h = blockIdx.y;
+  const int32_t* __restrict__ idx = idx_all + (size_t)h * R;
   for (int e = threadIdx.x; e < E; e += blockDim.x) cnt[e] = 0;
   __syncthreads();
   const int base = blockIdx.x * kChunk;
@@ -33,204 +85,192 @@ __global__ __launch_bounds__(256) void hist_kernel(const int32_t* __restrict__ i
     if (e >= 0 && e < E) atomicAdd(&cnt[e], 1);
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < E; e += blockDim.x)
-    block_counts[(size_t)blockIdx.x * E + e] = cnt[e];
+  int32_t* __restrict__ bc = block_counts_all + ((size_t)h * gridDim.x + blockIdx.x) * E;
+  for (int e = threadIdx.x; e < E; e += blockDim.x) bc[e] = cnt[e];
 }
 
-// Block counts are staged in LDS with coalesced loads (when they fit), so the
-// per-expert prefix over blocks reads LDS instead of a chain of dependent
-// global loads.
-constexpr int kScanStage = 8192;  // int32 entries of block counts staged in LDS
-
-__global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ block_counts,
-                                                   int nblk, int E,
-                                                   int32_t* __restrict__ counts,
-                                                   int32_t* __restrict__ offsets,
-                                                   int32_t* __restrict__ block_base, int row_base,
-                                                   int write_end) {
+// Past kFoldMax block counts: one workgroup per cluster writes the block
+// bases (expert offset + counts of the earlier blocks), offsets and counts.
+__global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ block_counts_all,
+                                                   int nblk, int E, int R,
+                                                   int32_t* __restrict__ counts_all,
+                                                   int32_t* __restrict__ offsets_all,
+                                                   int32_t* __restrict__ block_base_all) {
   __shared__ int total[kMaxE + 1];
-  __shared__ int staged[kScanStage];
+  const int h = blockIdx.x;
+  const int32_t* __restrict__ bc = block_counts_all + (size_t)h * nblk * E;
+  int32_t* __restrict__ bb = block_base_all + (size_t)h * nblk * E;
   const int e = threadIdx.x;
-  const int n = nblk * E;
-  const bool stage = n <= kScanStage;
-  if (stage)
-    for (int i = threadIdx.x; i < n; i += blockDim.x) staged[i] = block_counts[i];
-  __syncthreads();
   if (e < E) {
     int run = 0;
     for (int b = 0; b < nblk; ++b) {
-      const int c = stage ? staged[b * E + e] : block_counts[(size_t)b * E + e];
-      if (stage)
-        staged[b * E + e] = run;
-      else
-        block_base[(size_t)b * E + e] = run;
+      const int c = bc[(size_t)b * E + e];
+      bb[(size_t)b * E + e] = run;
       run += c;
     }
     total[e] = run;
   }
   __syncthreads();
-  // exclusive prefix over experts (E <= 256)
-  if (threadIdx.x == 0) {
-    int run = 0;
-    for (int i = 0; i < E; ++i) {
-      const int c = total[i];
-      total[i] = run;
-      run += c;
-    }
-    total[E] = run;
-  }
+  if (threadIdx.x < kWave) wave_excl_scan_experts(total, E);
   __syncthreads();
+  const int row_base = h * R;
   if (e < E) {
     const int off = total[e];
-    offsets[e] = row_base + off;
-    if (counts != nullptr) counts[e] = total[e + 1] - off;
+    offsets_all[(size_t)h * E + e] = row_base + off;
+    if (counts_all != nullptr) counts_all[(size_t)h * E + e] = total[e + 1] - off;
+    for (int b = 0; b < nblk; ++b) bb[(size_t)b * E + e] += off;
   }
-  if (e == 0 && write_end) offsets[E] = row_base + total[E];
-  // block bases (coalesced stores)
-  if (stage) {
-    for (int i = threadIdx.x; i < n; i += blockDim.x) block_base[i] = staged[i] + total[i % E];
-  } else if (e < E) {
-    for (int b = 0; b < nblk; ++b) block_base[(size_t)b * E + e] += total[e];
-  }
+  if (e == 0 && h == (int)gridDim.x - 1) offsets_all[(size_t)(h + 1) * E] = row_base + total[E];
 }
 
-__global__ __launch_bounds__(256) void rank_kernel(const int32_t* __restrict__ idx, int R, int E,
-                                                   const int32_t* __restrict__ block_base,
-                                                   int32_t* __restrict__ sorted_src,
-                                                   int32_t* __restrict__ row_of, int row_base) {
-  __shared__ int wcnt[kWavesP][kMaxE];
-  const int lane = lane_id();
-  const int wave = threadIdx.x >> 6;
-  for (int i = threadIdx.x; i < kWavesP * kMaxE; i += blockDim.x) (&wcnt[0][0])[i] = 0;
+template <bool FOLD>
+__global__ __launch_bounds__(kChunk) void rank_kernel(
+    const int32_t* __restrict__ idx_all, int R, int E, int nbits,
+    const int32_t* __restrict__ block_counts_all, const int32_t* __restrict__ block_base_all,
+    int32_t* __restrict__ counts_all, int32_t* __restrict__ offsets_all,
+    int32_t* __restrict__ sorted_src_all, int32_t* __restrict__ row_of_all) {
+  __shared__ int wcnt[kRankWaves][kMaxE];
+  __shared__ int total[kMaxE + 1];
+  __shared__ int before[kMaxE];
+  const int h = blockIdx.y;
+  const int nblk = gridDim.x;
+  const int row_base = h * R;
+  const int32_t* __restrict__ idx = idx_all + (size_t)h * R;
+  int32_t* __restrict__ sorted_src = sorted_src_all + (size_t)h * R;
+  int32_t* __restrict__ row_of = row_of_all + (size_t)h * R;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  for (int i = tid; i < kRankWaves * kMaxE; i += kChunk) (&wcnt[0][0])[i] = 0;
+  if (FOLD && tid < E) total[tid] = before[tid] = 0;
   __syncthreads();
 
-  const int start = blockIdx.x * kChunk + wave * kPerWave;
-  const int end = min(start + kPerWave, R);
-  // 1) per-wave counts of its contiguous sub-range
-  for (int f = start + lane; f < end; f += kWave) {
-    const int e = idx[f];
-    if (e >= 0 && e < E) atomicAdd(&wcnt[wave][e], 1);
+  const int f = blockIdx.x * kChunk + tid;
+  const bool valid = f < R;
+  const int e = valid ? idx[f] : -1;
+  const bool ok = valid && e >= 0 && e < E;
+  const uint64_t m = match_expert(e, ok, nbits);
+  const int r = __popcll(m & lanes_below());
+  if (ok && r == 0) wcnt[wave][e] = __popcll(m);
+
+  if (FOLD) {
+    // per-expert totals and counts of the earlier blocks, split over
+    // kChunk / E parts of the block list
+    const int32_t* __restrict__ bc = block_counts_all + (size_t)h * nblk * E;
+    const int parts = kChunk / E;
+    const int pe = tid % E, part = tid / E;
+    if (part < parts) {
+      int all = 0, bef = 0;
+      for (int b = part; b < nblk; b += parts) {
+        const int c = bc[(size_t)b * E + pe];
+        all += c;
+        bef += b < (int)blockIdx.x ? c : 0;
+      }
+      atomicAdd(&total[pe], all);
+      atomicAdd(&before[pe], bef);
+    }
+    __syncthreads();
+    if (tid < kWave) wave_excl_scan_experts(total, E);
   }
   __syncthreads();
-  // 2) per-wave base = block base + counts of the earlier waves (in place)
-  for (int e = threadIdx.x; e < E; e += blockDim.x) {
-    int run = block_base[(size_t)blockIdx.x * E + e];
-    for (int w = 0; w < kWavesP; ++w) {
-      const int c = wcnt[w][e];
-      wcnt[w][e] = run;
+  if (FOLD && blockIdx.x == 0) {
+    if (tid < E) {
+      offsets_all[(size_t)h * E + tid] = row_base + total[tid];
+      if (counts_all != nullptr) counts_all[(size_t)h * E + tid] = total[tid + 1] - total[tid];
+    }
+    if (tid == 0 && h == (int)gridDim.y - 1) offsets_all[(size_t)(h + 1) * E] = row_base + total[E];
+  }
+  // per-wave base = expert offset + earlier blocks + earlier waves (in place)
+  if (tid < E) {
+    int run = FOLD ? total[tid] + before[tid]
+                   : block_base_all[((size_t)h * nblk + blockIdx.x) * E + tid];
+#pragma unroll
+    for (int w = 0; w < kRankWaves; ++w) {
+      const int c = wcnt[w][tid];
+      wcnt[w][tid] = run;
       run += c;
     }
   }
   __syncthreads();
-  // 3) ranks in flat order, 64 pairs at a time
-  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int f0 = start; f0 < end; f0 += kWave) {
-    const int f = f0 + lane;
-    const bool valid = f < end;
-    const int e = valid ? idx[f] : -1;
-    const bool ok = valid && e >= 0 && e < E;
-    if (valid && !ok) row_of[f] = -1;
-    uint64_t remaining = __ballot(ok);
-    while (remaining) {
-      const int leader = __builtin_ctzll(remaining);
-      const int v = __builtin_amdgcn_readlane(e, leader);
-      const uint64_t m = __ballot(ok && e == v);
-      const int base = wcnt[wave][v];
-      if (ok && e == v) {
-        const int p = base + __popcll(m & lt_mask);
-        sorted_src[p] = f;
-        row_of[f] = row_base + p;
-      }
-      if (lane == leader) wcnt[wave][v] = base + __popcll(m);
-      remaining &= ~m;
-    }
+  if (ok) {
+    const int p = wcnt[wave][e] + r;
+    sorted_src[p] = f;
+    row_of[f] = row_base + p;
+  } else if (valid) {
+    row_of[f] = -1;
   }
 }
 
-// Small R: histogram, scan and stable ranks in one workgroup of 16 waves;
-// workgroup h handles cluster h (ids idx + h*R, outputs at h*R / h*E, rows
-// numbered from row_base = h*R).  Wave w owns the contiguous pairs
-// [w*per, (w+1)*per); per-wave counts give every wave its base per expert,
-// then each wave ranks its pairs in flat order with the same ballot walk as
-// rank_kernel.  The last workgroup writes the final offset.
+// Small R: histogram, prefix sum and stable ranks in one workgroup of 16
+// waves per cluster.  Wave w owns the contiguous range [w*per, (w+1)*per);
+// its per-chunk match masks give per-wave counts, then every wave ranks its
+// pairs in flat order, 64 at a time.
 constexpr int kSmallWaves = 16;
 constexpr int kSmallMaxR = 8192;
 
 __global__ __launch_bounds__(kSmallWaves * 64) void index_small_kernel(
-    const int32_t* __restrict__ idx_all, int R, int E, int32_t* __restrict__ counts_all,
-    int32_t* __restrict__ offsets_all, int32_t* __restrict__ sorted_src_all,
-    int32_t* __restrict__ row_of_all) {
+    const int32_t* __restrict__ idx_all, int R, int E, int nbits,
+    int32_t* __restrict__ counts_all, int32_t* __restrict__ offsets_all,
+    int32_t* __restrict__ sorted_src_all, int32_t* __restrict__ row_of_all) {
   const int h = blockIdx.x;
   const int row_base = h * R;
   const int32_t* __restrict__ idx = idx_all + (size_t)h * R;
-  int32_t* __restrict__ counts = counts_all != nullptr ? counts_all + (size_t)h * E : nullptr;
-  int32_t* __restrict__ offsets = offsets_all + (size_t)h * E;
   int32_t* __restrict__ sorted_src = sorted_src_all + (size_t)h * R;
   int32_t* __restrict__ row_of = row_of_all + (size_t)h * R;
   __shared__ int wcnt[kSmallWaves][kMaxE];
   __shared__ int total[kMaxE + 1];
-  const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
   for (int i = threadIdx.x; i < kSmallWaves * kMaxE; i += blockDim.x) (&wcnt[0][0])[i] = 0;
   __syncthreads();
   const int per = (R + kSmallWaves * kWave - 1) / (kSmallWaves * kWave) * kWave;
   const int start = wave * per;
   const int end = min(start + per, R);
-  for (int f = start + lane; f < end; f += kWave) {
-    const int e = idx[f];
-    if (e >= 0 && e < E) atomicAdd(&wcnt[wave][e], 1);
-  }
-  __syncthreads();
-  if (threadIdx.x < E) {
-    const int e = threadIdx.x;
-    int run = 0;
-    for (int w = 0; w < kSmallWaves; ++w) run += wcnt[w][e];
-    total[e] = run;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int run = 0;
-    for (int i = 0; i < E; ++i) {
-      const int c = total[i];
-      total[i] = run;
-      run += c;
-    }
-    total[E] = run;
-  }
-  __syncthreads();
-  if (threadIdx.x < E) {
-    const int e = threadIdx.x;
-    int run = total[e];
-    offsets[e] = row_base + run;
-    if (counts != nullptr) counts[e] = total[e + 1] - run;
-    for (int w = 0; w < kSmallWaves; ++w) {
-      const int c = wcnt[w][e];
-      wcnt[w][e] = run;
-      run += c;
-    }
-  }
-  if (threadIdx.x == 0 && h == (int)gridDim.x - 1) offsets[E] = row_base + total[E];
-  __syncthreads();
-  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const uint64_t below = lanes_below();
   for (int f0 = start; f0 < end; f0 += kWave) {
-    const int f = f0 + lane;
+    const int f = f0 + lane_id();
+    const int e = f < end ? idx[f] : -1;
+    const bool ok = e >= 0 && e < E;
+    const uint64_t m = match_expert(e, ok, nbits);
+    if (ok && __popcll(m & below) == 0) wcnt[wave][e] += __popcll(m);
+  }
+  __syncthreads();
+  if (threadIdx.x < E) {
+    int run = 0;
+    for (int w = 0; w < kSmallWaves; ++w) run += wcnt[w][threadIdx.x];
+    total[threadIdx.x] = run;
+  }
+  __syncthreads();
+  if (threadIdx.x < kWave) wave_excl_scan_experts(total, E);
+  __syncthreads();
+  if (threadIdx.x < E) {
+    const int ex = threadIdx.x;
+    int run = total[ex];
+    offsets_all[(size_t)h * E + ex] = row_base + run;
+    if (counts_all != nullptr) counts_all[(size_t)h * E + ex] = total[ex + 1] - run;
+    for (int w = 0; w < kSmallWaves; ++w) {
+      const int c = wcnt[w][ex];
+      wcnt[w][ex] = run;
+      run += c;
+    }
+  }
+  if (threadIdx.x == 0 && h == (int)gridDim.x - 1)
+    offsets_all[(size_t)(h + 1) * E] = row_base + total[E];
+  __syncthreads();
+  for (int f0 = start; f0 < end; f0 += kWave) {
+    const int f = f0 + lane_id();
     const bool valid = f < end;
     const int e = valid ? idx[f] : -1;
     const bool ok = valid && e >= 0 && e < E;
-    if (valid && !ok) row_of[f] = -1;
-    uint64_t remaining = __ballot(ok);
-    while (remaining) {
-      const int leader = __builtin_ctzll(remaining);
-      const int v = __builtin_amdgcn_readlane(e, leader);
-      const uint64_t m = __ballot(ok && e == v);
-      const int base = wcnt[wave][v];
-      if (ok && e == v) {
-        const int p = base + __popcll(m & lt_mask);
-        sorted_src[p] = f;
-        row_of[f] = row_base + p;
-      }
-      if (lane == leader) wcnt[wave][v] = base + __popcll(m);
-      remaining &= ~m;
+    const uint64_t m = match_expert(e, ok, nbits);
+    const int r = __popcll(m & below);
+    // every lane reads its base before the group's first lane advances it
+    // (a wave's LDS operations complete in order)
+    const int base = ok ? wcnt[wave][e] : 0;
+    if (ok) {
+      sorted_src[base + r] = f;
+      row_of[f] = row_base + base + r;
+      if (r == 0) wcnt[wave][e] = base + __popcll(m);
+    } else if (valid) {
+      row_of[f] = -1;
     }
   }
 }
@@ -275,9 +315,9 @@ __global__ void fill_i32_kernel(int32_t* p, int n, int32_t v) {
 
 int permute_blocks(int R) { return R > 0 ? ceil_div(R, kChunk) : 0; }
 
-size_t permute_scratch_bytes(int T, int k, int E) {
+size_t permute_scratch_bytes(int T, int k, int E, int C) {
   const size_t nblk = (size_t)permute_blocks(T * k);
-  return 2 * nblk * (size_t)E * sizeof(int32_t);
+  return 2 * (size_t)C * nblk * (size_t)E * sizeof(int32_t);
 }
 
 hipError_t launch_fill_i32(int32_t* p, int n, int32_t v, hipStream_t s) {
@@ -296,32 +336,34 @@ hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int
     if (err == hipSuccess && counts != nullptr) err = launch_fill_i32(counts, C * E, 0, s);
     return err;
   }
+  const int nbits = E <= 1 ? 0 : 32 - __builtin_clz((unsigned)(E - 1));
   if (R <= kSmallMaxR) {
     ProfileScope ps("permute_index", s);
     hipLaunchKernelGGL(index_small_kernel, dim3(C), dim3(kSmallWaves * kWave), 0, s, topk_idx, R,
-                       E, counts, offsets, sorted_src, row_of);
+                       E, nbits, counts, offsets, sorted_src, row_of);
     return hipGetLastError();
   }
   const int nblk = permute_blocks(R);
   int32_t* block_counts = reinterpret_cast<int32_t*>(scratch);
-  int32_t* block_base = block_counts + (size_t)nblk * E;
-  for (int h = 0; h < C; ++h) {
-    const int32_t* idx_h = topk_idx + (size_t)h * R;
-    {
-      ProfileScope ps("permute_hist", s);
-      hipLaunchKernelGGL(hist_kernel, dim3(nblk), dim3(256), 0, s, idx_h, R, E, block_counts);
-    }
-    {
-      ProfileScope ps("permute_scan", s);
-      hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(256), 0, s, block_counts, nblk, E,
-                         counts != nullptr ? counts + (size_t)h * E : nullptr,
-                         offsets + (size_t)h * E, block_base, h * R, h == C - 1 ? 1 : 0);
-    }
-    {
-      ProfileScope ps("permute_rank", s);
-      hipLaunchKernelGGL(rank_kernel, dim3(nblk), dim3(256), 0, s, idx_h, R, E, block_base,
-                         sorted_src + (size_t)h * R, row_of + (size_t)h * R, h * R);
-    }
+  int32_t* block_base = block_counts + (size_t)C * nblk * E;
+  {
+    ProfileScope ps("permute_hist", s);
+    hipLaunchKernelGGL(hist_kernel, dim3(nblk, C), dim3(256), 0, s, topk_idx, R, E, block_counts);
+  }
+  const bool fold = (size_t)nblk * E <= (size_t)kFoldMax;
+  if (!fold) {
+    ProfileScope ps("permute_scan", s);
+    hipLaunchKernelGGL(scan_kernel, dim3(C), dim3(256), 0, s, block_counts, nblk, E, R, counts,
+                       offsets, block_base);
+  }
+  {
+    ProfileScope ps("permute_rank", s);
+    if (fold)
+      hipLaunchKernelGGL(rank_kernel<true>, dim3(nblk, C), dim3(kChunk), 0, s, topk_idx, R, E,
+                         nbits, block_counts, block_base, counts, offsets, sorted_src, row_of);
+    else
+      hipLaunchKernelGGL(rank_kernel<false>, dim3(nblk, C), dim3(kChunk), 0, s, topk_idx, R, E,
+                         nbits, block_counts, block_base, counts, offsets, sorted_src, row_of);
   }
   return hipGetLastError();
 }

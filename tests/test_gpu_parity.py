@@ -176,6 +176,8 @@ def test_route_exact_ties_pick_lower_id(k):
     (8192, 2048, 16, 2, 1.2, (), "bf16"),
     (1025, 32, 256, 8, 0.5, (0, 255), "f32"),
     (5, 16, 4, 4, 0.0, (), "f32"),
+    (8800, 16, 256, 8, 0.8, (3,), "f32"),   # block counts past the in-rank sum
+    (9000, 16, 1, 1, 0.0, (), "f32"),       # E = 1 on the multi-block path
 ])
 def test_permute_parity(T, d, E, k, skew, dead, dt):
     say("permute", T, d, E, k, skew, dead, dt)
@@ -198,9 +200,10 @@ def test_permute_parity(T, d, E, k, skew, dead, dt):
     assert torch.equal(got["x_perm"], xd[ref_rows])
 
 
-def test_permute_drops_invalid_ids():
-    say("permute invalid ids")
-    T, d, E, k = 300, 64, 8, 2
+@pytest.mark.parametrize("T", [300, 6000])
+def test_permute_drops_invalid_ids(T):
+    say("permute invalid ids", T)
+    d, E, k = 64, 8, 2
     idx = synth.make_topk_idx(T, E, k, seed=5)
     idx[10, 1] = -1
     idx[200, 0] = E
@@ -377,6 +380,7 @@ def test_block_parity_sampled(name):
     (130, 64, 4, 2, 64, 2, 0.5, "f32", None),
     (200, 64, 100, 3, 64, 3, None, "bf16", None),    # 300 experts in one grouped FFN
     (600, 128, 64, 2, 128, 4, None, "bf16", None),    # 256 experts, large-tile path
+    (5000, 64, 8, 2, 64, 2, None, "bf16", None),      # two clusters, multi-block dispatch
 ])
 def test_block_parity_shapes(T, d, E, k, F, C, scale, dt, bias):
     say("block shapes", T, d, E, k, F, C, scale, dt, bias)
