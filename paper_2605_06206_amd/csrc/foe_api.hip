@@ -197,7 +197,7 @@ int foe_route(foe_dtype dt, int T, int d, int E, int k, const void* x, const voi
   c.small(topk_idx, any, "topk_idx");
   c.small(topk_w, any, "topk_w");
   if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_route: " + c.err);
-  hipError_t e = launch_route(dt, T, d, E, k, x, w_router, bias, topk_idx, topk_w,
+  hipError_t e = launch_route(dt, 1, T, d, E, k, x, w_router, bias, topk_idx, topk_w,
                               reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "foe_route");
   return FOE_OK;
@@ -347,19 +347,12 @@ int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F, co
   void* perm_ws = base + L.perm;
   void* ffn_ws = base + L.ffn;
 
-  const size_t s_el = esize(dt);
-  const size_t R = (size_t)T * k;
-  const unsigned char* wr = reinterpret_cast<const unsigned char*>(w_router);
-  // 1. routing of every cluster (Section 3.1: one score vector, per-group top-k)
-  for (int h = 0; h < C; ++h) {
-    hipError_t e = launch_route(dt, T, d, E, k, x, wr + (size_t)h * E * d * s_el,
-                                bias ? bias + (size_t)h * E : nullptr, topk_idx + h * R,
-                                topk_w + h * R, s);
-    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/route");
-  }
+  // 1. routing of every cluster in one grid (Section 3.1: one score vector,
+  //    per-group top-k)
+  hipError_t e = launch_route(dt, C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s);
+  if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/route");
   // 2. dispatch: expert histogram, prefix sum and stable ranks of all clusters
-  hipError_t e =
-      launch_index(T, E, k, C, topk_idx, counts, offsets, sorted_src, row_of, perm_ws, s);
+  e = launch_index(T, E, k, C, topk_idx, counts, offsets, sorted_src, row_of, perm_ws, s);
   if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/index");
   // 3. one grouped SwiGLU FFN over the C*E experts (weights are [C*E, ...]),
   //    reading the rows of x through sorted_src

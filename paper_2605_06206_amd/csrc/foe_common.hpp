@@ -76,7 +76,8 @@ inline int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 // ---- kernel launchers (one translation unit each) -------------------------
-hipError_t launch_route(foe_dtype dt, int T, int d, int E, int k, const void* x,
+// C clusters in one grid: w_router [C][E][d], bias [C][E], outputs [C][T][k]
+hipError_t launch_route(foe_dtype dt, int C, int T, int d, int E, int k, const void* x,
                         const void* w_router, const float* bias, int32_t* topk_idx,
                         float* topk_w, hipStream_t s);
 

@@ -128,6 +128,11 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
                                                         float* __restrict__ topk_w) {
   constexpr int UPW = (4 * TG + NW - 1) / NW;  // units per wave
   extern __shared__ __align__(16) unsigned char smem[];
+  // cluster blockIdx.y: its router matrix, bias and output rows
+  w += (size_t)blockIdx.y * E * d;
+  if (bias != nullptr) bias += (size_t)blockIdx.y * E;
+  topk_idx += (size_t)blockIdx.y * T_ * k;
+  topk_w += (size_t)blockIdx.y * T_ * k;
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
   const int t0 = blockIdx.x * kTok * TG;
@@ -233,6 +238,11 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
   __shared__ __align__(1024) unsigned char smem[NS * SB];
   __shared__ int sel_buf[WPB][8 * 32];
 
+  // cluster blockIdx.y: its router matrix, bias and output rows
+  w += (size_t)blockIdx.y * E * d;
+  if (bias != nullptr) bias += (size_t)blockIdx.y * E;
+  topk_idx += (size_t)blockIdx.y * T_ * k;
+  topk_w += (size_t)blockIdx.y * T_ * k;
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int t0 = (blockIdx.x * WPB + wave) * 16;  // this wave's tokens
@@ -354,12 +364,12 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
 }
 
 template <typename T, int NT, int NW, int TG>
-hipError_t launch_nt(int T_, int d, int E, int k, const void* x, const void* w,
+hipError_t launch_nt(int C, int T_, int d, int E, int k, const void* x, const void* w,
                      const float* bias, int32_t* idx, float* wt, hipStream_t s) {
   size_t lds_red = (size_t)NW * TG * NT * kWave * sizeof(f32x4);
   size_t lds_sel = (size_t)NW * 8 * k * 4;
   size_t lds = lds_red > lds_sel ? lds_red : lds_sel;
-  dim3 grid(ceil_div(T_, kTok * TG));
+  dim3 grid(ceil_div(T_, kTok * TG), C);
   ProfileScope ps("route", s);
   hipLaunchKernelGGL((route_kernel<T, NT, NW, TG>), grid, dim3(NW * kWave), lds, s,
                      reinterpret_cast<const T*>(x), reinterpret_cast<const T*>(w), bias, T_, d,
@@ -387,10 +397,10 @@ template <int TG_, int NW_> struct RouteCfg {
 #define FOE_ROUTE_TG32 2, 8
 #endif
 template <int WPB>
-hipError_t launch_stream(int T_, int d, int E, int k, const void* x, const void* w,
+hipError_t launch_stream(int C, int T_, int d, int E, int k, const void* x, const void* w,
                          const float* bias, int32_t* idx, float* wt, hipStream_t s) {
   constexpr int NS = 4;
-  dim3 grid(ceil_div(T_, 16 * WPB));
+  dim3 grid(ceil_div(T_, 16 * WPB), C);
   const bf16* xb = reinterpret_cast<const bf16*>(x);
   const bf16* wb = reinterpret_cast<const bf16*>(w);
   if (E <= 16)
@@ -403,8 +413,8 @@ hipError_t launch_stream(int T_, int d, int E, int k, const void* x, const void*
 }
 
 template <typename T>
-hipError_t launch_t(int T_, int d, int E, int k, const void* x, const void* w, const float* bias,
-                    int32_t* idx, float* wt, hipStream_t s) {
+hipError_t launch_t(int C, int T_, int d, int E, int k, const void* x, const void* w,
+                    const float* bias, int32_t* idx, float* wt, hipStream_t s) {
   const bool many = T_ >= 2048;
   if constexpr (sizeof(T) == 2) {
     // buffer offsets are 32-bit: x must span less than 2 GiB
@@ -414,31 +424,32 @@ hipError_t launch_t(int T_, int d, int E, int k, const void* x, const void* w, c
       // tokens for every CU
       ProfileScope ps("route", s);
       if (T_ >= 16384)
-        return launch_stream<4>(T_, d, E, k, x, w, bias, idx, wt, s);
-      return launch_stream<2>(T_, d, E, k, x, w, bias, idx, wt, s);
+        return launch_stream<4>(C, T_, d, E, k, x, w, bias, idx, wt, s);
+      return launch_stream<2>(C, T_, d, E, k, x, w, bias, idx, wt, s);
     }
   }
   if (E <= 16)
     return many ? launch_nt<T, 1, RouteCfg<FOE_ROUTE_TG16>::NW, RouteCfg<FOE_ROUTE_TG16>::TG>(
-                      T_, d, E, k, x, w, bias, idx, wt, s)
-                : launch_nt<T, 1, 8, 1>(T_, d, E, k, x, w, bias, idx, wt, s);
+                      C, T_, d, E, k, x, w, bias, idx, wt, s)
+                : launch_nt<T, 1, 8, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
   if (E <= 32)
     return many ? launch_nt<T, 2, RouteCfg<FOE_ROUTE_TG32>::NW, RouteCfg<FOE_ROUTE_TG32>::TG>(
-                      T_, d, E, k, x, w, bias, idx, wt, s)
-                : launch_nt<T, 2, 8, 1>(T_, d, E, k, x, w, bias, idx, wt, s);
-  if (E <= 64) return launch_nt<T, 4, 8, 1>(T_, d, E, k, x, w, bias, idx, wt, s);
-  if (E <= 128) return launch_nt<T, 8, 4, 1>(T_, d, E, k, x, w, bias, idx, wt, s);
-  return launch_nt<T, 16, 4, 1>(T_, d, E, k, x, w, bias, idx, wt, s);
+                      C, T_, d, E, k, x, w, bias, idx, wt, s)
+                : launch_nt<T, 2, 8, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
+  if (E <= 64) return launch_nt<T, 4, 8, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
+  if (E <= 128) return launch_nt<T, 8, 4, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
+  return launch_nt<T, 16, 4, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
 }
 
 }  // namespace
 
-hipError_t launch_route(foe_dtype dt, int T, int d, int E, int k, const void* x,
+hipError_t launch_route(foe_dtype dt, int C, int T, int d, int E, int k, const void* x,
                         const void* w_router, const float* bias, int32_t* topk_idx,
                         float* topk_w, hipStream_t s) {
-  if (T == 0) return hipSuccess;
-  if (dt == FOE_BF16) return launch_t<bf16>(T, d, E, k, x, w_router, bias, topk_idx, topk_w, s);
-  return launch_t<float>(T, d, E, k, x, w_router, bias, topk_idx, topk_w, s);
+  if (T == 0 || C == 0) return hipSuccess;
+  if (dt == FOE_BF16)
+    return launch_t<bf16>(C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s);
+  return launch_t<float>(C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s);
 }
 
 }  // namespace foe
