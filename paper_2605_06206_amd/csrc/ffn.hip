@@ -65,6 +65,9 @@
 #ifndef FOE_DECODE_STREAM
 #define FOE_DECODE_STREAM 1
 #endif
+#ifndef FOE_STREAM_ROT
+#define FOE_STREAM_ROT 1
+#endif
 #ifndef FOE_STREAM_NS
 #define FOE_STREAM_NS 3
 #endif
@@ -135,6 +138,15 @@ __device__ bool find_tile(const int32_t* __restrict__ offsets, int E, int rows, 
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
+
+// Calls f(integral_constant<int, I>) for I = B .. N-1 (compile-time indices).
+template <int B, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < N) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, N>(f);
+  }
+}
 
 // Source row of operand row r: r itself, or gather[r] / kdiv (-1 if that row
 // is outside [0, src_rows)).
@@ -906,9 +918,7 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
   const int e = blockIdx.x / gpe;
   if (e >= E) return;
   const int n0 = ((blockIdx.x % gpe) * WPB + wave) * NPW;
-  const int a = min(max(offsets[e], 0), rows);
-  const int b = max(min(max(offsets[e + 1], 0), rows), a);
-  if (b == a) return;  // uniform over the workgroup
+  const int off_a = offsets[e], off_b = offsets[e + 1];  // scalar loads, waited on below
   const uint32_t lds0 = lds_addr(smem);
 
   // weight sources: instruction i < 4 reads tile rows 4i.. of W0, i >= 4 rows
@@ -931,36 +941,81 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
     wv[i] = ((uint32_t)tr * K + q * 8) * 2u;
   }
   const int nks = (K + 127) / 128;
+  // Workgroups start their K walk at different chunks, so the reads in flight
+  // at any moment are spread over all column offsets of the 4 KB-strided
+  // weight rows (and so over the HBM channels) instead of one.
+  const int rot = FOE_STREAM_ROT ? (int)(blockIdx.x % (unsigned)nks) : 0;
+  auto chunk0 = [&](int kt) {
+    const int kc = kt + rot;
+    return (kc >= nks ? kc - nks : kc) * 128;
+  };
   // fragment read offsets inside a stage: row R of a 16-row tile
   const int R = lane & 15, g = lane >> 4;
   const int rbase = (R >> 2) * 1024 + (R & 3) * 256;
 
+  auto issue_w = [&](int kt, int s) {
+    const int k0 = chunk0(kt);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t off = k0 + wk[i] < K ? wv[i] + (uint32_t)k0 * 2u : kOob;
+      dma16(GATEUP && i >= 4 ? wr1 : wr0, off, lds0 + wave * WB, s * SB + i * 1024);
+    }
+  };
+  // The weights of the first NS-1 stages do not depend on the token rows:
+  // they go out before the segment bounds and gather indices are read.
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nks) issue_w(s, s);
+  const int a = min(max(off_a, 0), rows);
+  const int b = max(min(max(off_b, 0), rows), a);
+  if (b == a) {  // uniform over the workgroup; the DMAs land before LDS is released
+    vm_wait<0>();
+    return;
+  }
+
   for (int t0 = a; t0 < b; t0 += 32) {
     const int tv = min(32, b - t0);
-    // token instructions 2*wave and 2*wave+1 of this wave (rows 4i.. of the pass)
+    if (t0 != a) {
+#pragma unroll
+      for (int s = 0; s < NS - 1; ++s)
+        if (s < nks) issue_w(s, s);
+    }
+    // token instructions 2*wave and 2*wave+1 of this wave (rows 8*wave + 4u +
+    // lane/16 of the pass); the wave's 8 gather indices are uniform loads
     uint32_t xv[2];
     int xk[2];
+    {
+      const int tw = 8 * wave;
+      int gi[8];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int t = (2 * wave + u) * 4 + lr;
-      const int q = lc ^ (t & 15);
-      const int sr = t < tv ? src_row(gather, kdiv, t0 + t, a_rows) : -1;
-      xk[u] = q * 8;
-      xv[u] = sr < 0 ? kOob : ((uint32_t)sr * K + q * 8) * 2u;
-    }
-    auto issue = [&](int kt, int s) {
-      const int k0 = kt * 128;
+      for (int j = 0; j < 8; ++j)
+        gi[j] = (gather != nullptr && tw + j < tv) ? gather[t0 + tw + j] : t0 + tw + j;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const uint32_t off = k0 + wk[i] < K ? wv[i] + (uint32_t)k0 * 2u : kOob;
-        dma16(GATEUP && i >= 4 ? wr1 : wr0, off, lds0 + wave * WB, s * SB + i * 1024);
+      for (int u = 0; u < 2; ++u) {
+        const int t = tw + 4 * u + lr;
+        const int q = lc ^ (t & 15);
+        const int gsel = lr == 0 ? gi[4 * u] : lr == 1 ? gi[4 * u + 1] : lr == 2 ? gi[4 * u + 2]
+                                                                                 : gi[4 * u + 3];
+        int sr = -1;
+        if (t < tv) {
+          sr = gather == nullptr ? gsel : (gsel >= 0 ? gsel / kdiv : -1);
+          if (sr >= a_rows) sr = -1;
+        }
+        xk[u] = q * 8;
+        xv[u] = sr < 0 ? kOob : ((uint32_t)sr * K + q * 8) * 2u;
       }
+    }
+    auto issue_x = [&](int kt, int s) {
+      const int k0 = chunk0(kt);
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const uint32_t off = (k0 + xk[u] < K && xv[u] != kOob) ? xv[u] + (uint32_t)k0 * 2u : kOob;
         dma16(ar, off, lds0 + wave * 2048, s * SB + XB + u * 1024);
       }
     };
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+      if (s < nks) issue_x(s, s);
     f32x4 acc[2][2];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -969,13 +1024,20 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
 
     // iteration kt: wait for this wave's part of stage kt, meet the other
     // waves (stage kt complete, stage kt-1 no longer read), issue stage
-    // kt+NS-1 into the buffer of stage kt-1, use stage kt
-    auto body = [&](int kt, int s, int s_next) {
-      if (kt + NS - 2 < nks) vm_wait<NI * (NS - 2)>();
-      else vm_wait<0>();
+    // kt+NS-1 into the buffer of stage kt-1, use stage kt.  The pass starts
+    // with the weights of stages 0..NS-2 and then their token rows, so stage
+    // u < NS-1 still has 2*(NS-2-u) token and u*NI loop instructions behind it.
+    auto body = [&](int kt, auto U, int s_next) {
+      constexpr int u = decltype(U)::value;
+      if (kt + NS - 2 >= nks) vm_wait<0>();
+      else if (u < NS - 1 && kt == u) vm_wait<2 * (NS - 2 - u) + NI * u>();
+      else vm_wait<NI * (NS - 2)>();
       asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-      if (kt + NS - 1 < nks) issue(kt + NS - 1, s_next);
-      const unsigned char* src = smem + s * SB + rbase;
+      if (kt + NS - 1 < nks) {
+        issue_w(kt + NS - 1, s_next);
+        issue_x(kt + NS - 1, s_next);
+      }
+      const unsigned char* src = smem + u * SB + rbase;
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const int slot = ((c * 4 + g) ^ R) * 16;
@@ -989,15 +1051,12 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
         acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, x1, acc[1][1], 0, 0, 0);
       }
     };
-#pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
-      if (s < nks) issue(s, s);
     for (int kt0 = 0; kt0 < nks; kt0 += NS) {
-#pragma unroll
-      for (int u = 0; u < NS; ++u) {
+      static_for<0, NS>([&](auto U) {
+        constexpr int u = decltype(U)::value;
         const int kt = kt0 + u;
-        if (kt < nks) body(kt, u, (u + NS - 1) % NS);
-      }
+        if (kt < nks) body(kt, U, (u + NS - 1) % NS);
+      });
     }
     // every wave is done with the ring before the next pass refills it
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
