@@ -87,12 +87,14 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
 // with y holding the FFN rows of every cluster (row_of values index it
 // directly).  Evaluated as scale * (C * x[i] + S) where S sums the weighted
 // rows in the order (h = 0..C-1, j = 0..k-1) in fp32; the per-cluster partials
-// never reach HBM.
+// never reach HBM.  Without row_of, y is indexed by pair (h*T*k + i*k + j) and
+// a pair counts when its expert id in sel_all lies in [0, E).
 template <typename T>
 __global__ __launch_bounds__(256) void combine_clusters_kernel(
     const T* __restrict__ y, const int32_t* __restrict__ row_of_all,
-    const float* __restrict__ w_all, const T* __restrict__ x, int C, int T_, int d, int k,
-    int y_rows, float scale, T* __restrict__ out) {
+    const int32_t* __restrict__ sel_all, int E, const float* __restrict__ w_all,
+    const T* __restrict__ x, int C, int T_, int d, int k, int y_rows, float scale,
+    T* __restrict__ out) {
   constexpr int EPV = Vec16<T>::N;
   constexpr int U = FOE_COMBINE_U;
   const int lane = lane_id();
@@ -115,11 +117,16 @@ __global__ __launch_bounds__(256) void combine_clusters_kernel(
       if (c < nvec) xv[u] = load16(x + (size_t)tok * d + (size_t)c * EPV);
     }
     for (int h = 0; h < C; ++h) {
-      const int32_t* rows = row_of_all + h * R + (size_t)tok * k;
-      const float* wts = w_all + h * R + (size_t)tok * k;
+      const size_t pr = h * R + (size_t)tok * k;  // first pair of the token
+      const int32_t* rows = (row_of_all != nullptr ? row_of_all : sel_all) + pr;
+      const float* wts = w_all + pr;
       for (int j = 0; j < k; j += 2) {
         const bool two = j + 1 < k;
-        const int p0 = rows[j], p1 = two ? rows[j + 1] : -1;
+        int p0 = rows[j], p1 = two ? rows[j + 1] : -1;
+        if (row_of_all == nullptr) {
+          p0 = (p0 >= 0 && p0 < E) ? (int)pr + j : -1;
+          p1 = (p1 >= 0 && p1 < E) ? (int)pr + j + 1 : -1;
+        }
         const float w0 = wts[j], w1 = two ? wts[j + 1] : 0.f;
         const bool ok0 = p0 >= 0 && p0 < y_rows, ok1 = p1 >= 0 && p1 < y_rows;
         Vec16<T> v0[U], v1[U];
@@ -210,19 +217,20 @@ hipError_t launch_combine(foe_dtype dt, int T, int d, int k, const void* y_perm,
 
 hipError_t launch_combine_clusters(foe_dtype dt, int C, int T, int d, int k, const void* y,
                                    const int32_t* row_of_all, const float* w_all, const void* x,
-                                   float scale, void* out, hipStream_t s) {
+                                   float scale, void* out, hipStream_t s, const int32_t* sel_all,
+                                   int E) {
   if (T == 0) return hipSuccess;
   const int y_rows = C * T * k;
   dim3 grid(ceil_div(T, 4));
   ProfileScope ps("combine", s);
   if (dt == FOE_BF16)
     hipLaunchKernelGGL(combine_clusters_kernel<bf16>, grid, dim3(256), 0, s,
-                       reinterpret_cast<const bf16*>(y), row_of_all, w_all,
+                       reinterpret_cast<const bf16*>(y), row_of_all, sel_all, E, w_all,
                        reinterpret_cast<const bf16*>(x), C, T, d, k, y_rows, scale,
                        reinterpret_cast<bf16*>(out));
   else
     hipLaunchKernelGGL(combine_clusters_kernel<float>, grid, dim3(256), 0, s,
-                       reinterpret_cast<const float*>(y), row_of_all, w_all,
+                       reinterpret_cast<const float*>(y), row_of_all, sel_all, E, w_all,
                        reinterpret_cast<const float*>(x), C, T, d, k, y_rows, scale,
                        reinterpret_cast<float*>(out));
   return hipGetLastError();

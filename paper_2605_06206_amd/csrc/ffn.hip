@@ -65,6 +65,9 @@
 #ifndef FOE_DECODE_STREAM
 #define FOE_DECODE_STREAM 1
 #endif
+#ifndef FOE_FFN_SEL
+#define FOE_FFN_SEL 1
+#endif
 #ifndef FOE_STREAM_ROT
 #define FOE_STREAM_ROT 1
 #endif
@@ -80,6 +83,10 @@
 
 namespace foe {
 namespace {
+
+// Most (token, slot) pairs per cluster for which the decode FFN builds each
+// expert's pair list itself from the routing decisions.
+constexpr int kSelMax = 2048;
 
 template <int W, int U> struct FirstOf { static constexpr int value = W; };
 
@@ -897,11 +904,12 @@ __global__ __launch_bounds__(KW * 64) void ffn_skinny_bf16(
 // All loads of the loop are LDS DMA issued from inline assembly with explicit
 // vmcnt waits, so NS-2 later stages stay in flight while a stage is used.
 
-template <bool GATEUP, int NS>
+template <bool GATEUP, int NS, bool SEL>
 __global__ __launch_bounds__(256) void ffn_stream_bf16(
     const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv, int a_rows,
     const int32_t* __restrict__ offsets, int E, int rows, const bf16* __restrict__ W0,
-    const bf16* __restrict__ W1, int N, int K, bf16* __restrict__ out, int n_groups) {
+    const bf16* __restrict__ W1, int N, int K, bf16* __restrict__ out, int n_groups,
+    int e_per_c, int r_sel) {
   static_assert(NS >= 2 && NS <= 4, "2 to 4 stages");
   constexpr int WPB = 4;
   constexpr int NPW = GATEUP ? 16 : 32;  // output columns per wave
@@ -909,8 +917,10 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
   constexpr int XB = WPB * WB;            // offset of the token rows in a stage
   constexpr int SB = XB + 8192;           // bytes per stage
   constexpr int NI = 10;                  // DMA instructions per stage and wave
-  static_assert(NS * SB <= 160 * 1024, "LDS capacity");
-  __shared__ __align__(1024) unsigned char smem[NS * SB];
+  constexpr int SELB = SEL ? kSelMax * 4 : 0;       // staged expert ids of the cluster
+  constexpr int LSTB = SEL ? kSelMax * 4 + 64 : 0;  // pair list + wave counts
+  static_assert(NS * SB + SELB + LSTB <= 160 * 1024, "LDS capacity");
+  __shared__ __align__(1024) unsigned char smem[NS * SB + SELB + LSTB];
 
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
@@ -918,8 +928,22 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
   const int e = blockIdx.x / gpe;
   if (e >= E) return;
   const int n0 = ((blockIdx.x % gpe) * WPB + wave) * NPW;
-  const int off_a = offsets[e], off_b = offsets[e + 1];  // scalar loads, waited on below
+  int off_a = 0, off_b = 0;
+  if constexpr (!SEL) {
+    off_a = offsets[e];  // scalar loads, waited on below
+    off_b = offsets[e + 1];
+  }
+  // selection mode: expert e is expert le of cluster hc
+  const int hc = SEL ? e / e_per_c : 0;
+  const int le = SEL ? e - hc * e_per_c : 0;
   const uint32_t lds0 = lds_addr(smem);
+  if constexpr (SEL) {
+    // the cluster's r_sel expert ids go to LDS first (256 per wave instruction)
+    const __amdgpu_buffer_rsrc_t sr =
+        make_rsrc_u(gather + (size_t)hc * r_sel, (uint32_t)r_sel * 4u);
+    for (int c = wave * 256; c < r_sel; c += WPB * 256)
+      dma16(sr, (uint32_t)(c + 4 * lane) * 4u, lds0 + NS * SB + c * 4, 0);
+  }
 
   // weight sources: instruction i < 4 reads tile rows 4i.. of W0, i >= 4 rows
   // 4(i-4).. of W1 (gate/up) or rows 4i.. of W0 (down); a wave past N reads
@@ -966,8 +990,42 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
     if (s < nks) issue_w(s, s);
-  const int a = min(max(off_a, 0), rows);
-  const int b = max(min(max(off_b, 0), rows), a);
+  int a = 0, b = 0;
+  const int* lst = reinterpret_cast<const int*>(smem + NS * SB + SELB);
+  if constexpr (SEL) {
+    // Pair list of this expert in ascending pair order (the stable order of
+    // the dispatch): per 256-pair chunk, each wave ballots its matches and
+    // the wave counts give the positions.  The weight DMAs stay in flight.
+    if (nks >= NS - 1) vm_wait<8 * (NS - 1)>();
+    else vm_wait<0>();
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    const int* sel = reinterpret_cast<const int*>(smem + NS * SB);
+    int* lw = reinterpret_cast<int*>(smem + NS * SB + SELB);
+    int* wc = lw + kSelMax;
+    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+    int n = 0;
+    for (int c0 = 0; c0 < r_sel; c0 += WPB * 64) {
+      const int f = c0 + (int)threadIdx.x;
+      const bool ok = f < r_sel && sel[f] == le;
+      const uint64_t m = __ballot(ok);
+      if (lane == 0) wc[wave] = __popcll(m);
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      int pre = 0, tot = 0;
+#pragma unroll
+      for (int w = 0; w < WPB; ++w) {
+        const int cw = wc[w];
+        pre += w < wave ? cw : 0;
+        tot += cw;
+      }
+      if (ok) lw[n + pre + __popcll(m & below)] = f;
+      n += tot;
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    }
+    b = n;
+  } else {
+    a = min(max(off_a, 0), rows);
+    b = max(min(max(off_b, 0), rows), a);
+  }
   if (b == a) {  // uniform over the workgroup; the DMAs land before LDS is released
     vm_wait<0>();
     return;
@@ -984,7 +1042,21 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
     // lane/16 of the pass); the wave's 8 gather indices are uniform loads
     uint32_t xv[2];
     int xk[2];
-    {
+    if constexpr (SEL) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int t = 8 * wave + 4 * u + lr;
+        const int q = lc ^ (t & 15);
+        int sr = -1;
+        if (t < tv) {
+          const int f = lst[t0 + t];
+          sr = GATEUP ? f / kdiv : hc * r_sel + f;
+          if (sr >= a_rows) sr = -1;
+        }
+        xk[u] = q * 8;
+        xv[u] = sr < 0 ? kOob : ((uint32_t)sr * K + q * 8) * 2u;
+      }
+    } else {
       const int tw = 8 * wave;
       int gi[8];
 #pragma unroll
@@ -1067,7 +1139,8 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
     for (int j = 0; j < 2; ++j) {
       const int t = j * 16 + R;
       if (t >= tv) continue;
-      bf16* orow = out + (size_t)(t0 + t) * N + n0;
+      const int orow_i = SEL ? hc * r_sel + lst[t0 + t] : t0 + t;
+      bf16* orow = out + (size_t)orow_i * N + n0;
       if constexpr (GATEUP) {
         if (nb < nv) {
           bf16x4 o;
@@ -1090,6 +1163,7 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
 }
 
 constexpr int kSkinnyWaves = FirstOf<FOE_SKINNY>::value;
+
 
 // ---- fp32 path: plain FMA kernels (small shapes) ---------------------------
 __device__ int expert_of_row(const int32_t* __restrict__ offsets, int E, int rows, int row) {
@@ -1230,16 +1304,16 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
     {
       const int ng = ceil_div(F, 16);
       ProfileScope ps("ffn_gateup", s);
-      hipLaunchKernelGGL((ffn_stream_bf16<true, FOE_STREAM_NS>), dim3(E * ceil_div(ng, 4)),
+      hipLaunchKernelGGL((ffn_stream_bf16<true, FOE_STREAM_NS, false>), dim3(E * ceil_div(ng, 4)),
                          dim3(256), 0, s, xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F,
-                         d, h, ng);
+                         d, h, ng, 1, 0);
     }
     {
       const int ng = ceil_div(d, 32);
       ProfileScope ps("ffn_down", s);
-      hipLaunchKernelGGL((ffn_stream_bf16<false, FOE_STREAM_NS>), dim3(E * ceil_div(ng, 4)),
-                         dim3(256), 0, s, static_cast<const bf16*>(h), nullptr, 1, rows, offsets,
-                         E, rows, wd, nullptr, d, F, y, ng);
+      hipLaunchKernelGGL((ffn_stream_bf16<false, FOE_STREAM_NS, false>),
+                         dim3(E * ceil_div(ng, 4)), dim3(256), 0, s, static_cast<const bf16*>(h),
+                         nullptr, 1, rows, offsets, E, rows, wd, nullptr, d, F, y, ng, 1, 0);
     }
   } else if (rows < 64 * E && FOE_DECODE_DMA) {
     DmaLaunch<FOE_DMA_GU_DEC>::run<true>(xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F, d,
@@ -1275,6 +1349,41 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
     launch_gemm<FOE_PIPE_DN, false, FOE_PIPE_OPT>(h, nullptr, 1, rows, offsets, E, rows, wd,
                                                   nullptr, d, F, y, s, "ffn_down");
 #endif
+  }
+  return hipGetLastError();
+}
+
+bool ffn_sel_ok(foe_dtype dt, int C, int E, int T, int k) {
+  const long long R = (long long)T * k;
+  return FOE_FFN_SEL && FOE_DECODE_STREAM && dt == FOE_BF16 && R > 0 && R <= kSelMax &&
+         (long long)C * R < 64LL * C * E;
+}
+
+hipError_t launch_expert_ffn_sel(int C, int E, int d, int F, int T, int k, const void* x,
+                                 const int32_t* topk_idx, const void* w_gate, const void* w_up,
+                                 const void* w_down, void* y, void* scratch, hipStream_t s) {
+  const int R = T * k;
+  const int rows = C * R;
+  const bf16* xa = static_cast<const bf16*>(x);
+  const bf16* wg = static_cast<const bf16*>(w_gate);
+  const bf16* wu = static_cast<const bf16*>(w_up);
+  const bf16* wd = static_cast<const bf16*>(w_down);
+  bf16* h = static_cast<bf16*>(scratch);
+  bf16* yo = static_cast<bf16*>(y);
+  {
+    const int ng = ceil_div(F, 16);
+    ProfileScope ps("ffn_gateup", s);
+    hipLaunchKernelGGL((ffn_stream_bf16<true, FOE_STREAM_NS, true>), dim3(C * E * ceil_div(ng, 4)),
+                       dim3(256), 0, s, xa, topk_idx, k, T, nullptr, C * E, rows, wg, wu, F, d, h,
+                       ng, E, R);
+  }
+  {
+    const int ng = ceil_div(d, 32);
+    ProfileScope ps("ffn_down", s);
+    hipLaunchKernelGGL((ffn_stream_bf16<false, FOE_STREAM_NS, true>),
+                       dim3(C * E * ceil_div(ng, 4)), dim3(256), 0, s,
+                       static_cast<const bf16*>(h), topk_idx, 1, rows, nullptr, C * E, rows, wd,
+                       nullptr, d, F, yo, ng, E, R);
   }
   return hipGetLastError();
 }

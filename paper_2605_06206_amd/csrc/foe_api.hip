@@ -351,6 +351,17 @@ int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F, co
   //    per-group top-k)
   hipError_t e = launch_route(dt, C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s);
   if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/route");
+  if (ffn_sel_ok(dt, C, E, T, k)) {
+    // few pairs per expert: the FFN workgroups list their expert's pairs from
+    // the routing decisions themselves (the dispatch in its stable order,
+    // without an index pass) and y is indexed by pair
+    e = launch_expert_ffn_sel(C, E, d, F, T, k, x, topk_idx, w_gate, w_up, w_down, y, ffn_ws, s);
+    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/expert_ffn");
+    e = launch_combine_clusters(dt, C, T, d, k, y, nullptr, topk_w, x, reduce_scale, out, s,
+                                topk_idx, E);
+    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/combine");
+    return FOE_OK;
+  }
   // 2. dispatch: expert histogram, prefix sum and stable ranks of all clusters
   e = launch_index(T, E, k, C, topk_idx, counts, offsets, sorted_src, row_of, perm_ws, s);
   if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/index");

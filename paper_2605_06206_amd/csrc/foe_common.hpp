@@ -104,9 +104,21 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
                                 const int32_t* gather, int kdiv, int a_rows,
                                 const int32_t* offsets, const void* w_gate, const void* w_up,
                                 const void* w_down, void* y_perm, void* scratch, hipStream_t s);
+// Decode form of the block's FFN (bf16, few pairs per expert): every
+// workgroup lists its expert's pairs from the routing decisions topk_idx
+// [C][T*k] itself (no dispatch index pass); the intermediate rows and the
+// output rows y [C*T*k][d] are indexed by pair.  ffn_sel_ok() tells whether
+// the shape takes this form.
+bool ffn_sel_ok(foe_dtype dt, int C, int E, int T, int k);
+hipError_t launch_expert_ffn_sel(int C, int E, int d, int F, int T, int k, const void* x,
+                                 const int32_t* topk_idx, const void* w_gate, const void* w_up,
+                                 const void* w_down, void* y, void* scratch, hipStream_t s);
+// row_of_all == nullptr: y row of pair p of cluster h is h*T*k + p, skipped
+// when the expert id sel_all[h*T*k + p] is outside [0, E)
 hipError_t launch_combine_clusters(foe_dtype dt, int C, int T, int d, int k, const void* y,
                                    const int32_t* row_of_all, const float* w_all, const void* x,
-                                   float scale, void* out, hipStream_t s);
+                                   float scale, void* out, hipStream_t s,
+                                   const int32_t* sel_all = nullptr, int E = 0);
 hipError_t launch_combine(foe_dtype dt, int T, int d, int k, const void* y_perm,
                           const int32_t* row_of, const float* topk_w, const void* residual,
                           void* out, hipStream_t s);
