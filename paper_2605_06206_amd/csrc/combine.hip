@@ -98,12 +98,17 @@ __global__ __launch_bounds__(256) void combine_clusters_kernel(
   constexpr int EPV = Vec16<T>::N;
   constexpr int U = FOE_COMBINE_U;
   const int lane = lane_id();
-  const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (tok >= T_) return;
   const size_t R = (size_t)T_ * k;
   const int nvec = d / EPV;
+  // one wave per (token, chunk of U*64 vectors): many short waves keep a
+  // small batch's few dependent loads in flight together
+  const int nch = (nvec + U * kWave - 1) / (U * kWave);
+  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int tok = wid / nch;
+  if (tok >= T_) return;
   const float cx = (float)C;
-  for (int c0 = 0; c0 < nvec; c0 += U * kWave) {
+  {
+    const int c0 = (wid - tok * nch) * U * kWave;
     float acc[U][EPV];
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -122,19 +127,31 @@ __global__ __launch_bounds__(256) void combine_clusters_kernel(
       const float* wts = w_all + pr;
       for (int j = 0; j < k; j += 2) {
         const bool two = j + 1 < k;
-        int p0 = rows[j], p1 = two ? rows[j + 1] : -1;
-        if (row_of_all == nullptr) {
-          p0 = (p0 >= 0 && p0 < E) ? (int)pr + j : -1;
-          p1 = (p1 >= 0 && p1 < E) ? (int)pr + j + 1 : -1;
+        const bool by_pair = row_of_all == nullptr;
+        int p0, p1;
+        bool ok0, ok1;
+        if (by_pair) {
+          // the y row of every pair exists: its loads need not wait for the
+          // expert ids, which only decide whether it counts
+          p0 = (int)pr + j;
+          p1 = two ? p0 + 1 : -1;
+          const int e0 = rows[j], e1 = two ? rows[j + 1] : -1;
+          ok0 = e0 >= 0 && e0 < E;
+          ok1 = two && e1 >= 0 && e1 < E;
+        } else {
+          p0 = rows[j];
+          p1 = two ? rows[j + 1] : -1;
+          ok0 = p0 >= 0 && p0 < y_rows;
+          ok1 = p1 >= 0 && p1 < y_rows;
         }
         const float w0 = wts[j], w1 = two ? wts[j + 1] : 0.f;
-        const bool ok0 = p0 >= 0 && p0 < y_rows, ok1 = p1 >= 0 && p1 < y_rows;
         Vec16<T> v0[U], v1[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           const int c = c0 + u * kWave + lane;
-          if (c < nvec && ok0) v0[u] = load16(y + (size_t)p0 * d + (size_t)c * EPV);
-          if (c < nvec && ok1) v1[u] = load16(y + (size_t)p1 * d + (size_t)c * EPV);
+          if (c < nvec && (by_pair || ok0)) v0[u] = load16(y + (size_t)p0 * d + (size_t)c * EPV);
+          if (c < nvec && (by_pair ? two : ok1))
+            v1[u] = load16(y + (size_t)p1 * d + (size_t)c * EPV);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -221,7 +238,9 @@ hipError_t launch_combine_clusters(foe_dtype dt, int C, int T, int d, int k, con
                                    int E) {
   if (T == 0) return hipSuccess;
   const int y_rows = C * T * k;
-  dim3 grid(ceil_div(T, 4));
+  const int nvec = d / (dt == FOE_BF16 ? 8 : 4);
+  const long long nch = ceil_div(nvec, FOE_COMBINE_U * kWave);
+  dim3 grid(ceil_div((long long)T * nch, 4));
   ProfileScope ps("combine", s);
   if (dt == FOE_BF16)
     hipLaunchKernelGGL(combine_clusters_kernel<bf16>, grid, dim3(256), 0, s,

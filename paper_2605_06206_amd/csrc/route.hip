@@ -39,7 +39,7 @@ template <typename T> struct RouteMma;
 // One W_r fragment serves the TG token groups of the workgroup.
 template <> struct RouteMma<bf16> {
   static constexpr int KSTEP = 32;
-  template <int NT, int NW, int TG>
+  template <int NT, int NW, int TG, int KB>
   __device__ static void run(const bf16* x, const bf16* w, int T, int d, int E, int t0,
                              int wave, int lane, f32x4 (&acc)[TG][NT]) {
     const int r = lane & 15, q = lane >> 4;
@@ -52,11 +52,11 @@ template <> struct RouteMma<bf16> {
       xrow[g] = x + (size_t)(tok_ok[g] ? tok : 0) * d;
     }
     const int nsteps = (d + KSTEP - 1) / KSTEP;
-    // wave w takes K-step groups w, w+NW, ... of kBatch steps each
-    for (int c0 = wave * kBatch; c0 < nsteps; c0 += NW * kBatch) {
-      u32x4 a[kBatch][TG], b[kBatch][NT];
+    // wave w takes K-step groups w, w+NW, ... of KB steps each
+    for (int c0 = wave * KB; c0 < nsteps; c0 += NW * KB) {
+      u32x4 a[KB][TG], b[KB][NT];
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
+      for (int u = 0; u < KB; ++u) {
         const int kb = (c0 + u) * KSTEP + q * 8;
         const bool k_ok = c0 + u < nsteps && kb < d;
 #pragma unroll
@@ -71,7 +71,7 @@ template <> struct RouteMma<bf16> {
                                         : zero_u32x4();
       }
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u)
+      for (int u = 0; u < KB; ++u)
 #pragma unroll
         for (int g = 0; g < TG; ++g)
 #pragma unroll
@@ -87,7 +87,7 @@ template <> struct RouteMma<bf16> {
 // s-th using element s (k map kc + 4q + s on both operands).
 template <> struct RouteMma<float> {
   static constexpr int KSTEP = 16;
-  template <int NT, int NW, int TG>
+  template <int NT, int NW, int TG, int KB>
   __device__ static void run(const float* x, const float* w, int T, int d, int E, int t0,
                              int wave, int lane, f32x4 (&acc)[TG][NT]) {
     const int r = lane & 15, q = lane >> 4;
@@ -119,7 +119,7 @@ template <> struct RouteMma<float> {
 // A "unit" is accumulator register i of token group g: in the 16x16 MFMA
 // layout it holds tokens g*16 + 4*(lane/16) + i (one per 16-lane row) and
 // experts nt*16 + lane%16.  The 4*TG units are spread over the waves.
-template <typename T, int NT, int NW, int TG>
+template <typename T, int NT, int NW, int TG, int KB>
 __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
                                                         const T* __restrict__ w,
                                                         const float* __restrict__ bias, int T_,
@@ -142,7 +142,7 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
   for (int g = 0; g < TG; ++g)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[g][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  RouteMma<T>::template run<NT, NW, TG>(x, w, T_, d, E, t0, wave, lane, acc);
+  RouteMma<T>::template run<NT, NW, TG, KB>(x, w, T_, d, E, t0, wave, lane, acc);
 
   // partial tiles of the NW waves -> LDS [wave][g][nt][lane] (f32x4)
   f32x4* part = reinterpret_cast<f32x4*>(smem);
@@ -363,7 +363,7 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
   }
 }
 
-template <typename T, int NT, int NW, int TG>
+template <typename T, int NT, int NW, int TG, int KB = kBatch>
 hipError_t launch_nt(int C, int T_, int d, int E, int k, const void* x, const void* w,
                      const float* bias, int32_t* idx, float* wt, hipStream_t s) {
   size_t lds_red = (size_t)NW * TG * NT * kWave * sizeof(f32x4);
@@ -371,7 +371,7 @@ hipError_t launch_nt(int C, int T_, int d, int E, int k, const void* x, const vo
   size_t lds = lds_red > lds_sel ? lds_red : lds_sel;
   dim3 grid(ceil_div(T_, kTok * TG), C);
   ProfileScope ps("route", s);
-  hipLaunchKernelGGL((route_kernel<T, NT, NW, TG>), grid, dim3(NW * kWave), lds, s,
+  hipLaunchKernelGGL((route_kernel<T, NT, NW, TG, KB>), grid, dim3(NW * kWave), lds, s,
                      reinterpret_cast<const T*>(x), reinterpret_cast<const T*>(w), bias, T_, d,
                      E, k, idx, wt);
   return hipGetLastError();
