@@ -62,7 +62,9 @@ def parse():
 
 
 # kernel name (library timing hooks) -> source file that holds it
-KERNEL_SOURCES = {"route": "route.hip", "index": "permute.hip", "permute": "permute.hip",
+KERNEL_SOURCES = {"route": "route.hip", "permute_index": "permute.hip",
+                  "permute_hist": "permute.hip", "permute_rank": "permute.hip",
+                  "permute_scan": "permute.hip", "permute_scatter": "permute.hip",
                   "ffn_gateup": "ffn.hip", "ffn_down": "ffn.hip", "ffn_gateup_f32": "ffn.hip",
                   "ffn_down_f32": "ffn.hip", "combine": "combine.hip", "reduce": "combine.hip"}
 
@@ -103,15 +105,18 @@ def copy_calibration():
 
 def kernel_work(name, cfg, e_touched):
     """Algorithmic (flops, bytes) of ONE launch of kernel `name` in a
-    foe_cluster_block step.  Route runs once per cluster; the index pass, the
-    two grouped FFN kernels (all C*E experts) and the combine + reduction run
-    once per step.  `e_touched` = experts (over all clusters) that got rows."""
+    foe_cluster_block step.  Every kernel runs once per step over all C
+    clusters: routing, the index pass (absent when the decode FFN lists its
+    experts' pairs itself), the two grouped FFN kernels (all C*E experts) and
+    the combine + reduction.  `e_touched` = experts (over all clusters) that
+    got rows."""
     T, d, E, k, F, C = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["F"], cfg["C"]
     s = 2 if cfg["dtype"] == "bf16" else 4
     R = T * k          # pairs per cluster
     CR = C * R         # permuted rows over all clusters
     if name == "route":
-        return 2.0 * T * d * E, T * d * s + E * d * s + 8.0 * R
+        # x once, every cluster's router matrix, (idx, w) per pair
+        return 2.0 * C * T * d * E, T * d * s + C * E * d * s + 8.0 * CR
     if name in ("ffn_gateup", "ffn_gateup_f32"):
         return 4.0 * CR * d * F, 2.0 * e_touched * F * d * s + CR * d * s + CR * F * s
     if name in ("ffn_down", "ffn_down_f32"):

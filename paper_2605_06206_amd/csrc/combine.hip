@@ -220,12 +220,12 @@ hipError_t launch_combine(foe_dtype dt, int T, int d, int k, const void* y_perm,
   dim3 grid(ceil_div(T, 4));
   ProfileScope ps("combine", s);
   if (dt == FOE_BF16)
-    hipLaunchKernelGGL(combine_kernel<bf16>, grid, dim3(256), 0, s,
+    FOE_LAUNCH(combine_kernel<bf16>, grid, dim3(256), 0, s,
                        reinterpret_cast<const bf16*>(y_perm), row_of, topk_w,
                        reinterpret_cast<const bf16*>(residual), T, d, k,
                        reinterpret_cast<bf16*>(out));
   else
-    hipLaunchKernelGGL(combine_kernel<float>, grid, dim3(256), 0, s,
+    FOE_LAUNCH(combine_kernel<float>, grid, dim3(256), 0, s,
                        reinterpret_cast<const float*>(y_perm), row_of, topk_w,
                        reinterpret_cast<const float*>(residual), T, d, k,
                        reinterpret_cast<float*>(out));
@@ -243,12 +243,12 @@ hipError_t launch_combine_clusters(foe_dtype dt, int C, int T, int d, int k, con
   dim3 grid(ceil_div((long long)T * nch, 4));
   ProfileScope ps("combine", s);
   if (dt == FOE_BF16)
-    hipLaunchKernelGGL(combine_clusters_kernel<bf16>, grid, dim3(256), 0, s,
+    FOE_LAUNCH(combine_clusters_kernel<bf16>, grid, dim3(256), 0, s,
                        reinterpret_cast<const bf16*>(y), row_of_all, sel_all, E, w_all,
                        reinterpret_cast<const bf16*>(x), C, T, d, k, y_rows, scale,
                        reinterpret_cast<bf16*>(out));
   else
-    hipLaunchKernelGGL(combine_clusters_kernel<float>, grid, dim3(256), 0, s,
+    FOE_LAUNCH(combine_clusters_kernel<float>, grid, dim3(256), 0, s,
                        reinterpret_cast<const float*>(y), row_of_all, sel_all, E, w_all,
                        reinterpret_cast<const float*>(x), C, T, d, k, y_rows, scale,
                        reinterpret_cast<float*>(out));
@@ -264,12 +264,12 @@ hipError_t launch_reduce(foe_dtype dt, int C, int T, int d, const void* partials
   dim3 grid((unsigned)(want < 8192 ? want : 8192));
   ProfileScope ps("reduce", s);
   if (dt == FOE_BF16)
-    hipLaunchKernelGGL(reduce_kernel<bf16>, grid, dim3(256), 0, s,
+    FOE_LAUNCH(reduce_kernel<bf16>, grid, dim3(256), 0, s,
                        reinterpret_cast<const bf16*>(partials),
                        reinterpret_cast<const bf16*>(residual), scale, C, nvec, plane,
                        reinterpret_cast<bf16*>(out));
   else
-    hipLaunchKernelGGL(reduce_kernel<float>, grid, dim3(256), 0, s,
+    FOE_LAUNCH(reduce_kernel<float>, grid, dim3(256), 0, s,
                        reinterpret_cast<const float*>(partials),
                        reinterpret_cast<const float*>(residual), scale, C, nvec, plane,
                        reinterpret_cast<float*>(out));

@@ -1225,7 +1225,7 @@ void launch_gemm(const bf16* A, const int32_t* gather, int kdiv, int a_rows,
   const long long n_tiles = (long long)max_mt * ntn;
   dim3 grid((unsigned)((n_tiles + 7) / 8 * 8));
   ProfileScope ps(name, s);
-  hipLaunchKernelGGL((grouped_gemm_bf16<BM, BN, WM, WN, GATEUP, NSETS, MAXW>), grid,
+  FOE_LAUNCH((grouped_gemm_bf16<BM, BN, WM, WN, GATEUP, NSETS, MAXW>), grid,
                      dim3(WM * WN * kWave), 0, s, A, gather, kdiv, a_rows, offsets, E, rows, B0,
                      B1, N, K, out, ntn, (int)n_tiles);
 }
@@ -1253,7 +1253,7 @@ void launch_gemm_dma(const bf16* A, const int32_t* gather, int kdiv, int a_rows,
   }
   dim3 grid((unsigned)nb);
   ProfileScope ps(name, s);
-  hipLaunchKernelGGL((grouped_gemm_dma<BM, BN, WM, WN, GATEUP, BK, NST, PW, GM, PERSIST != 0>), grid,
+  FOE_LAUNCH((grouped_gemm_dma<BM, BN, WM, WN, GATEUP, BK, NST, PW, GM, PERSIST != 0>), grid,
                      dim3(WM * WN * kWave), 0, s, A, gather, kdiv, a_rows, offsets, E, rows, B0,
                      B1, N, K, out, ntn, (int)n_tiles);
 }
@@ -1281,14 +1281,14 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
     float* h = reinterpret_cast<float*>(scratch);
     {
       ProfileScope ps("ffn_gateup_f32", s);
-      hipLaunchKernelGGL(gateup_f32, dim3(ceil_div((long long)rows * F, 256)), dim3(256), 0, s,
+      FOE_LAUNCH(gateup_f32, dim3(ceil_div((long long)rows * F, 256)), dim3(256), 0, s,
                          reinterpret_cast<const float*>(A), gather, kdiv, a_rows, offsets, E,
                          rows, reinterpret_cast<const float*>(w_gate),
                          reinterpret_cast<const float*>(w_up), F, d, h);
     }
     {
       ProfileScope ps("ffn_down_f32", s);
-      hipLaunchKernelGGL(down_f32, dim3(ceil_div((long long)rows * d, 256)), dim3(256), 0, s, h,
+      FOE_LAUNCH(down_f32, dim3(ceil_div((long long)rows * d, 256)), dim3(256), 0, s, h,
                          offsets, E, rows, reinterpret_cast<const float*>(w_down), d, F,
                          reinterpret_cast<float*>(y_perm));
     }
@@ -1304,14 +1304,14 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
     {
       const int ng = ceil_div(F, 16);
       ProfileScope ps("ffn_gateup", s);
-      hipLaunchKernelGGL((ffn_stream_bf16<true, FOE_STREAM_NS, false>), dim3(E * ceil_div(ng, 4)),
+      FOE_LAUNCH((ffn_stream_bf16<true, FOE_STREAM_NS, false>), dim3(E * ceil_div(ng, 4)),
                          dim3(256), 0, s, xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F,
                          d, h, ng, 1, 0);
     }
     {
       const int ng = ceil_div(d, 32);
       ProfileScope ps("ffn_down", s);
-      hipLaunchKernelGGL((ffn_stream_bf16<false, FOE_STREAM_NS, false>),
+      FOE_LAUNCH((ffn_stream_bf16<false, FOE_STREAM_NS, false>),
                          dim3(E * ceil_div(ng, 4)), dim3(256), 0, s, static_cast<const bf16*>(h),
                          nullptr, 1, rows, offsets, E, rows, wd, nullptr, d, F, y, ng, 1, 0);
     }
@@ -1325,14 +1325,14 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
     {
       const int ng = ceil_div(F, 16);
       ProfileScope ps("ffn_gateup", s);
-      hipLaunchKernelGGL((ffn_skinny_bf16<true, FOE_SKINNY>), dim3(E * ng),
+      FOE_LAUNCH((ffn_skinny_bf16<true, FOE_SKINNY>), dim3(E * ng),
                          dim3(kSkinnyWaves * kWave), 0, s, xa, gather, kdiv, a_rows, offsets, E,
                          rows, wg, wu, F, d, h, ng);
     }
     {
       const int ng = ceil_div(d, 32);
       ProfileScope ps("ffn_down", s);
-      hipLaunchKernelGGL((ffn_skinny_bf16<false, FOE_SKINNY>), dim3(E * ng),
+      FOE_LAUNCH((ffn_skinny_bf16<false, FOE_SKINNY>), dim3(E * ng),
                          dim3(kSkinnyWaves * kWave), 0, s, h, nullptr, 1, rows, offsets, E, rows,
                          wd, nullptr, d, F, y, ng);
     }
@@ -1373,14 +1373,14 @@ hipError_t launch_expert_ffn_sel(int C, int E, int d, int F, int T, int k, const
   {
     const int ng = ceil_div(F, 16);
     ProfileScope ps("ffn_gateup", s);
-    hipLaunchKernelGGL((ffn_stream_bf16<true, FOE_STREAM_NS, true>), dim3(C * E * ceil_div(ng, 4)),
+    FOE_LAUNCH((ffn_stream_bf16<true, FOE_STREAM_NS, true>), dim3(C * E * ceil_div(ng, 4)),
                        dim3(256), 0, s, xa, topk_idx, k, T, nullptr, C * E, rows, wg, wu, F, d, h,
                        ng, E, R);
   }
   {
     const int ng = ceil_div(d, 32);
     ProfileScope ps("ffn_down", s);
-    hipLaunchKernelGGL((ffn_stream_bf16<false, FOE_STREAM_NS, true>),
+    FOE_LAUNCH((ffn_stream_bf16<false, FOE_STREAM_NS, true>),
                        dim3(C * E * ceil_div(ng, 4)), dim3(256), 0, s,
                        static_cast<const bf16*>(h), topk_idx, 1, rows, nullptr, C * E, rows, wd,
                        nullptr, d, F, yo, ng, E, R);

@@ -114,7 +114,7 @@ std::vector<ProfRec> g_recs;
 
 }  // namespace
 
-int profile_begin(const char* name, hipStream_t stream) {
+int profile_begin(const char* name) {
   std::lock_guard<std::mutex> lock(g_prof_mu);
   if (!g_prof_on) return -1;
   if (g_events_used * 2 + 2 > g_events.size()) {
@@ -129,14 +129,18 @@ int profile_begin(const char* name, hipStream_t stream) {
   }
   const int ev = (int)g_events_used++;
   g_recs.push_back({name, ev});
-  (void)hipEventRecord(g_events[2 * ev], stream);
   return ev;
 }
 
-void profile_end(int slot, hipStream_t stream) {
-  if (slot < 0) return;
+hipEvent_t profile_event(int slot, int stop) {
+  if (slot < 0) return nullptr;
   std::lock_guard<std::mutex> lock(g_prof_mu);
-  (void)hipEventRecord(g_events[2 * slot + 1], stream);
+  return g_events[2 * slot + (stop ? 1 : 0)];
+}
+
+int& profile_cur_slot() {
+  static thread_local int slot = -1;
+  return slot;
 }
 
 }  // namespace foe

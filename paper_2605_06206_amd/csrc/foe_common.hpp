@@ -1,6 +1,7 @@
 // Shared device/host helpers of the gfx950 per-cluster MoE block library.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -60,17 +61,28 @@ __device__ __forceinline__ int row_ror(int v) {
 }
 
 // ---- host side: launch bookkeeping ----------------------------------------
-// Kernel timing hooks (see foe_profile_* in foe.h).  `begin` returns an opaque
-// slot index or -1 when timing is off; `end` closes it.
-int profile_begin(const char* name, hipStream_t stream);
-void profile_end(int slot, hipStream_t stream);
+// Kernel timing hooks (see foe_profile_* in foe.h).  A ProfileScope names the
+// one launch it encloses; while timing is on, `profile_begin` hands it a slot
+// with an event pair and FOE_LAUNCH passes that pair to hipExtLaunchKernelGGL,
+// which stamps the events with the dispatch's own start and end (the interval
+// holds the kernel alone, not the launch latency before it).
+int profile_begin(const char* name);
+hipEvent_t profile_event(int slot, int stop);
+int& profile_cur_slot();  // slot of this thread's innermost live scope, -1 none
 
 struct ProfileScope {
-  int slot;
-  hipStream_t stream;
-  ProfileScope(const char* name, hipStream_t s) : slot(profile_begin(name, s)), stream(s) {}
-  ~ProfileScope() { profile_end(slot, stream); }
+  int slot, prev;
+  ProfileScope(const char* name, hipStream_t)
+      : slot(profile_begin(name)), prev(profile_cur_slot()) {
+    profile_cur_slot() = slot;
+  }
+  ~ProfileScope() { profile_cur_slot() = prev; }
 };
+
+#define FOE_LAUNCH(kernel, grid, block, lds, stream, ...)                                     \
+  hipExtLaunchKernelGGL(kernel, grid, block, lds, stream,                                   \
+                        ::foe::profile_event(::foe::profile_cur_slot(), 0),                 \
+                        ::foe::profile_event(::foe::profile_cur_slot(), 1), 0u, __VA_ARGS__)
 
 inline int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }

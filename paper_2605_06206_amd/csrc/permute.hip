@@ -323,7 +323,7 @@ size_t permute_scratch_bytes(int T, int k, int E, int C) {
 hipError_t launch_fill_i32(int32_t* p, int n, int32_t v, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   ProfileScope ps("fill_i32", s);
-  hipLaunchKernelGGL(fill_i32_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, p, n, v);
+  FOE_LAUNCH(fill_i32_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, p, n, v);
   return hipGetLastError();
 }
 
@@ -339,7 +339,7 @@ hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int
   const int nbits = E <= 1 ? 0 : 32 - __builtin_clz((unsigned)(E - 1));
   if (R <= kSmallMaxR) {
     ProfileScope ps("permute_index", s);
-    hipLaunchKernelGGL(index_small_kernel, dim3(C), dim3(kSmallWaves * kWave), 0, s, topk_idx, R,
+    FOE_LAUNCH(index_small_kernel, dim3(C), dim3(kSmallWaves * kWave), 0, s, topk_idx, R,
                        E, nbits, counts, offsets, sorted_src, row_of);
     return hipGetLastError();
   }
@@ -348,21 +348,21 @@ hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int
   int32_t* block_base = block_counts + (size_t)C * nblk * E;
   {
     ProfileScope ps("permute_hist", s);
-    hipLaunchKernelGGL(hist_kernel, dim3(nblk, C), dim3(256), 0, s, topk_idx, R, E, block_counts);
+    FOE_LAUNCH(hist_kernel, dim3(nblk, C), dim3(256), 0, s, topk_idx, R, E, block_counts);
   }
   const bool fold = (size_t)nblk * E <= (size_t)kFoldMax;
   if (!fold) {
     ProfileScope ps("permute_scan", s);
-    hipLaunchKernelGGL(scan_kernel, dim3(C), dim3(256), 0, s, block_counts, nblk, E, R, counts,
+    FOE_LAUNCH(scan_kernel, dim3(C), dim3(256), 0, s, block_counts, nblk, E, R, counts,
                        offsets, block_base);
   }
   {
     ProfileScope ps("permute_rank", s);
     if (fold)
-      hipLaunchKernelGGL(rank_kernel<true>, dim3(nblk, C), dim3(kChunk), 0, s, topk_idx, R, E,
+      FOE_LAUNCH(rank_kernel<true>, dim3(nblk, C), dim3(kChunk), 0, s, topk_idx, R, E,
                          nbits, block_counts, block_base, counts, offsets, sorted_src, row_of);
     else
-      hipLaunchKernelGGL(rank_kernel<false>, dim3(nblk, C), dim3(kChunk), 0, s, topk_idx, R, E,
+      FOE_LAUNCH(rank_kernel<false>, dim3(nblk, C), dim3(kChunk), 0, s, topk_idx, R, E,
                          nbits, block_counts, block_base, counts, offsets, sorted_src, row_of);
   }
   return hipGetLastError();
@@ -378,11 +378,11 @@ hipError_t launch_permute(foe_dtype dt, int T, int d, int E, int k, const int32_
   ProfileScope ps("permute_scatter", s);
   dim3 grid(ceil_div(T, 4));
   if (dt == FOE_BF16)
-    hipLaunchKernelGGL(scatter_rows_kernel<bf16>, grid, dim3(256), 0, s,
+    FOE_LAUNCH(scatter_rows_kernel<bf16>, grid, dim3(256), 0, s,
                        reinterpret_cast<const bf16*>(x), row_of, T, d, k, R,
                        reinterpret_cast<bf16*>(x_perm));
   else
-    hipLaunchKernelGGL(scatter_rows_kernel<float>, grid, dim3(256), 0, s,
+    FOE_LAUNCH(scatter_rows_kernel<float>, grid, dim3(256), 0, s,
                        reinterpret_cast<const float*>(x), row_of, T, d, k, R,
                        reinterpret_cast<float*>(x_perm));
   return hipGetLastError();

@@ -371,7 +371,7 @@ hipError_t launch_nt(int C, int T_, int d, int E, int k, const void* x, const vo
   size_t lds = lds_red > lds_sel ? lds_red : lds_sel;
   dim3 grid(ceil_div(T_, kTok * TG), C);
   ProfileScope ps("route", s);
-  hipLaunchKernelGGL((route_kernel<T, NT, NW, TG, KB>), grid, dim3(NW * kWave), lds, s,
+  FOE_LAUNCH((route_kernel<T, NT, NW, TG, KB>), grid, dim3(NW * kWave), lds, s,
                      reinterpret_cast<const T*>(x), reinterpret_cast<const T*>(w), bias, T_, d,
                      E, k, idx, wt);
   return hipGetLastError();
@@ -390,6 +390,9 @@ template <int TG_, int NW_> struct RouteCfg {
 #ifndef FOE_ROUTE_STREAM_MIN_T
 #define FOE_ROUTE_STREAM_MIN_T 8192
 #endif
+#ifndef FOE_ROUTE_SMALL_NW
+#define FOE_ROUTE_SMALL_NW 8
+#endif
 #ifndef FOE_ROUTE_TG16
 #define FOE_ROUTE_TG16 1, 8
 #endif
@@ -404,10 +407,10 @@ hipError_t launch_stream(int C, int T_, int d, int E, int k, const void* x, cons
   const bf16* xb = reinterpret_cast<const bf16*>(x);
   const bf16* wb = reinterpret_cast<const bf16*>(w);
   if (E <= 16)
-    hipLaunchKernelGGL((route_stream_kernel<1, NS, WPB>), grid, dim3(WPB * kWave), 0, s, xb, wb,
+    FOE_LAUNCH((route_stream_kernel<1, NS, WPB>), grid, dim3(WPB * kWave), 0, s, xb, wb,
                        bias, T_, d, E, k, idx, wt);
   else
-    hipLaunchKernelGGL((route_stream_kernel<2, NS, WPB>), grid, dim3(WPB * kWave), 0, s, xb, wb,
+    FOE_LAUNCH((route_stream_kernel<2, NS, WPB>), grid, dim3(WPB * kWave), 0, s, xb, wb,
                        bias, T_, d, E, k, idx, wt);
   return hipGetLastError();
 }
@@ -431,11 +434,11 @@ hipError_t launch_t(int C, int T_, int d, int E, int k, const void* x, const voi
   if (E <= 16)
     return many ? launch_nt<T, 1, RouteCfg<FOE_ROUTE_TG16>::NW, RouteCfg<FOE_ROUTE_TG16>::TG>(
                       C, T_, d, E, k, x, w, bias, idx, wt, s)
-                : launch_nt<T, 1, 8, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
+                : launch_nt<T, 1, FOE_ROUTE_SMALL_NW, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
   if (E <= 32)
     return many ? launch_nt<T, 2, RouteCfg<FOE_ROUTE_TG32>::NW, RouteCfg<FOE_ROUTE_TG32>::TG>(
                       C, T_, d, E, k, x, w, bias, idx, wt, s)
-                : launch_nt<T, 2, 8, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
+                : launch_nt<T, 2, FOE_ROUTE_SMALL_NW, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
   if (E <= 64) return launch_nt<T, 4, 8, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
   if (E <= 128) return launch_nt<T, 8, 4, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
   return launch_nt<T, 16, 4, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
