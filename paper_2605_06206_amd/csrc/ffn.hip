@@ -87,6 +87,8 @@ namespace {
 // Most (token, slot) pairs per cluster for which the decode FFN builds each
 // expert's pair list itself from the routing decisions.
 constexpr int kSelMax = 2048;
+constexpr int kScDevice = 16;  // buffer cache policy SC1: device-scope coherence
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 template <int W, int U> struct FirstOf { static constexpr int value = W; };
 
@@ -909,7 +911,7 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
     const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv, int a_rows,
     const int32_t* __restrict__ offsets, int E, int rows, const bf16* __restrict__ W0,
     const bf16* __restrict__ W1, int N, int K, bf16* __restrict__ out, int n_groups,
-    int e_per_c, int r_sel) {
+    int e_per_c, int r_sel, FusedCombine fc) {
   static_assert(NS >= 2 && NS <= 4, "2 to 4 stages");
   constexpr int WPB = 4;
   constexpr int NPW = GATEUP ? 16 : 32;  // output columns per wave
@@ -954,6 +956,8 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
   const __amdgpu_buffer_rsrc_t wr1 =
       GATEUP ? make_rsrc_u(W1 + wrow * K, (uint32_t)nv * K * 2u) : wr0;
   const __amdgpu_buffer_rsrc_t ar = make_rsrc_u(A, (uint32_t)a_rows * K * 2u);
+  // output rows of the folded combine (down, selection mode)
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc_u(out, (uint32_t)rows * N * 2u);
   const int lr = lane >> 4, lc = lane & 15;
   uint32_t wv[8];  // byte offset of this lane's weight chunk in instruction i (stage 0)
   int wk[8];       // its K column
@@ -1155,7 +1159,68 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
           bf16x4 o;
 #pragma unroll
           for (int v = 0; v < 4; ++v) o[v] = (bf16)acc[i][j][v];
-          *reinterpret_cast<bf16x4*>(orow + i * 16 + nb) = o;
+          if (SEL && fc.out != nullptr)  // device-scope store: read back by other workgroups
+            __builtin_amdgcn_raw_buffer_store_b64(
+                __builtin_bit_cast(u32x2, o), yr,
+                (uint32_t)(((size_t)orow_i * N + n0 + i * 16 + nb) * 2), 0, kScDevice);
+          else
+            *reinterpret_cast<bf16x4*>(orow + i * 16 + nb) = o;
+        }
+      }
+    }
+  }
+
+  if constexpr (!GATEUP && SEL) {
+    if (fc.out != nullptr) {
+      // Combine folded in: this workgroup's y columns [cg*128, +128) of its
+      // pairs are stored (device-scope stores, past the XCD's own L2, and
+      // acknowledged once visible to every XCD); count one arrival per (token,
+      // column group).  The workgroup that brings a count to C*k forms that
+      // token's output columns from device-scope loads of the y rows, summing
+      // the k rows of every cluster in the fixed order (h, j) exactly as the
+      // combine kernel does.  Nothing waits on another workgroup.
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      const int cg = blockIdx.x % gpe;
+      int* done = reinterpret_cast<int*>(smem + NS * SB);  // staged ids are dead
+      int* ndone = reinterpret_cast<int*>(smem + NS * SB + SELB) + kSelMax;
+      if (threadIdx.x == 0) *ndone = 0;
+      __syncthreads();
+      const int need = fc.C * fc.k;
+      for (int i = (int)threadIdx.x; i < b; i += WPB * 64) {
+        const int t = lst[i] / fc.k;
+        const int old = atomicAdd(&fc.cnt[(size_t)t * gpe + cg], 1);
+        if (old == need - 1) done[atomicAdd(ndone, 1)] = t;
+      }
+      __syncthreads();
+      const int nd = *ndone;
+      if (nd > 0) {
+        const int c0 = cg * 128;
+        const int nvec = (min(128, N - c0) + 7) / 8;
+        const float cx = (float)fc.C;
+        for (int it = (int)threadIdx.x; it < nd * 16; it += WPB * 64) {
+          const int v = it & 15;
+          if (v >= nvec) continue;
+          const int t = done[it >> 4];
+          const int col = c0 + v * 8;
+          float acc[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+          for (int h = 0; h < fc.C; ++h) {
+            for (int j = 0; j < fc.k; ++j) {
+              const size_t p = (size_t)h * r_sel + (size_t)t * fc.k + j;
+              const float wj = fc.w[p];
+              const bf16x8 yv = __builtin_bit_cast(
+                  bf16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                              yr, (uint32_t)((p * N + col) * 2), 0, kScDevice));
+#pragma unroll
+              for (int q = 0; q < 8; ++q) acc[q] = fmaf(wj, (float)yv[q], acc[q]);
+            }
+          }
+          const bf16x8 xv = *reinterpret_cast<const bf16x8*>(fc.x + (size_t)t * N + col);
+          bf16x8 o;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) o[q] = (bf16)(fc.scale * fmaf(cx, (float)xv[q], acc[q]));
+          *reinterpret_cast<bf16x8*>(fc.out + (size_t)t * N + col) = o;
         }
       }
     }
@@ -1306,14 +1371,15 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
       ProfileScope ps("ffn_gateup", s);
       FOE_LAUNCH((ffn_stream_bf16<true, FOE_STREAM_NS, false>), dim3(E * ceil_div(ng, 4)),
                          dim3(256), 0, s, xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F,
-                         d, h, ng, 1, 0);
+                         d, h, ng, 1, 0, FusedCombine{});
     }
     {
       const int ng = ceil_div(d, 32);
       ProfileScope ps("ffn_down", s);
       FOE_LAUNCH((ffn_stream_bf16<false, FOE_STREAM_NS, false>),
                          dim3(E * ceil_div(ng, 4)), dim3(256), 0, s, static_cast<const bf16*>(h),
-                         nullptr, 1, rows, offsets, E, rows, wd, nullptr, d, F, y, ng, 1, 0);
+                         nullptr, 1, rows, offsets, E, rows, wd, nullptr, d, F, y, ng, 1, 0,
+                         FusedCombine{});
     }
   } else if (rows < 64 * E && FOE_DECODE_DMA) {
     DmaLaunch<FOE_DMA_GU_DEC>::run<true>(xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F, d,
@@ -1361,7 +1427,8 @@ bool ffn_sel_ok(foe_dtype dt, int C, int E, int T, int k) {
 
 hipError_t launch_expert_ffn_sel(int C, int E, int d, int F, int T, int k, const void* x,
                                  const int32_t* topk_idx, const void* w_gate, const void* w_up,
-                                 const void* w_down, void* y, void* scratch, hipStream_t s) {
+                                 const void* w_down, void* y, void* scratch, hipStream_t s,
+                                 const FusedCombine& fc) {
   const int R = T * k;
   const int rows = C * R;
   const bf16* xa = static_cast<const bf16*>(x);
@@ -1375,7 +1442,7 @@ hipError_t launch_expert_ffn_sel(int C, int E, int d, int F, int T, int k, const
     ProfileScope ps("ffn_gateup", s);
     FOE_LAUNCH((ffn_stream_bf16<true, FOE_STREAM_NS, true>), dim3(C * E * ceil_div(ng, 4)),
                        dim3(256), 0, s, xa, topk_idx, k, T, nullptr, C * E, rows, wg, wu, F, d, h,
-                       ng, E, R);
+                       ng, E, R, FusedCombine{});
   }
   {
     const int ng = ceil_div(d, 32);
@@ -1383,7 +1450,7 @@ hipError_t launch_expert_ffn_sel(int C, int E, int d, int F, int T, int k, const
     FOE_LAUNCH((ffn_stream_bf16<false, FOE_STREAM_NS, true>),
                        dim3(C * E * ceil_div(ng, 4)), dim3(256), 0, s,
                        static_cast<const bf16*>(h), topk_idx, 1, rows, nullptr, C * E, rows, wd,
-                       nullptr, d, F, yo, ng, E, R);
+                       nullptr, d, F, yo, ng, E, R, fc);
   }
   return hipGetLastError();
 }

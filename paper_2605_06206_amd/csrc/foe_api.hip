@@ -76,7 +76,7 @@ bool operand_fits(long long rows, long long cols, size_t el) {
 // clusters consecutively (cluster h from h*T*k); one grouped FFN runs over the
 // C*E experts reading x through sorted_src; one kernel combines and reduces.
 struct BlockWs {
-  size_t topk_idx, topk_w, counts, offsets, sorted_src, row_of, y, perm, ffn, total;
+  size_t topk_idx, topk_w, counts, offsets, sorted_src, row_of, y, perm, ffn, cnt, total;
 };
 
 BlockWs block_ws(foe_dtype dt, int C, int T, int d, int E, int k, int F) {
@@ -97,6 +97,7 @@ BlockWs block_ws(foe_dtype dt, int C, int T, int d, int E, int k, int F) {
   take(w.y, CR * d * s);
   take(w.perm, permute_scratch_bytes(T, k, E, C));
   take(w.ffn, ffn_scratch_bytes(dt, (int)CR, F));
+  take(w.cnt, (size_t)T * ceil_div(d, 128) * 4);  // folded-combine arrival counters
   w.total = align_up(off, 256);
   return w;
 }
@@ -353,17 +354,28 @@ int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F, co
 
   // 1. routing of every cluster in one grid (Section 3.1: one score vector,
   //    per-group top-k)
-  hipError_t e = launch_route(dt, C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s);
+  const bool sel = ffn_sel_ok(dt, C, E, T, k);
+  hipError_t e = launch_route(dt, C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s,
+                              sel ? reinterpret_cast<int32_t*>(base + L.cnt) : nullptr,
+                              ceil_div(d, 128));
   if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/route");
-  if (ffn_sel_ok(dt, C, E, T, k)) {
+  if (sel) {
     // few pairs per expert: the FFN workgroups list their expert's pairs from
     // the routing decisions themselves (the dispatch in its stable order,
-    // without an index pass) and y is indexed by pair
-    e = launch_expert_ffn_sel(C, E, d, F, T, k, x, topk_idx, w_gate, w_up, w_down, y, ffn_ws, s);
+    // without an index pass), y is indexed by pair, and the down kernel also
+    // forms the combine (its arrival counters were cleared by the route
+    // kernel above; every token has C*k valid pairs since k <= E)
+    FusedCombine fc;
+    fc.w = topk_w;
+    fc.x = static_cast<const bf16*>(x);
+    fc.out = static_cast<bf16*>(out);
+    fc.cnt = reinterpret_cast<int32_t*>(base + L.cnt);
+    fc.scale = reduce_scale;
+    fc.C = C;
+    fc.k = k;
+    e = launch_expert_ffn_sel(C, E, d, F, T, k, x, topk_idx, w_gate, w_up, w_down, y, ffn_ws, s,
+                              fc);
     if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/expert_ffn");
-    e = launch_combine_clusters(dt, C, T, d, k, y, nullptr, topk_w, x, reduce_scale, out, s,
-                                topk_idx, E);
-    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/combine");
     return FOE_OK;
   }
   // 2. dispatch: expert histogram, prefix sum and stable ranks of all clusters

@@ -88,10 +88,12 @@ inline int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 // ---- kernel launchers (one translation unit each) -------------------------
-// C clusters in one grid: w_router [C][E][d], bias [C][E], outputs [C][T][k]
+// C clusters in one grid: w_router [C][E][d], bias [C][E], outputs [C][T][k].
+// zero_cnt != nullptr: the kernel also clears zero_cnt[T][zero_per_tok].
 hipError_t launch_route(foe_dtype dt, int C, int T, int d, int E, int k, const void* x,
                         const void* w_router, const float* bias, int32_t* topk_idx,
-                        float* topk_w, hipStream_t s);
+                        float* topk_w, hipStream_t s, int32_t* zero_cnt = nullptr,
+                        int zero_per_tok = 0);
 
 // permute scratch = 2 * C * nblk * E int32 (see permute_blocks())
 int permute_blocks(int R);
@@ -116,6 +118,19 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
                                 const int32_t* gather, int kdiv, int a_rows,
                                 const int32_t* offsets, const void* w_gate, const void* w_up,
                                 const void* w_down, void* y_perm, void* scratch, hipStream_t s);
+// The block's combine folded into the decode down kernel: w = topk_w [C][T*k],
+// x and out [T][d], cnt = [T][ceil(d/128)] arrival counters that must be zero
+// when the down kernel starts (the route kernel of the same call clears them).
+// out == nullptr: not folded.
+struct FusedCombine {
+  const float* w = nullptr;
+  const bf16* x = nullptr;
+  bf16* out = nullptr;
+  int32_t* cnt = nullptr;
+  float scale = 1.f;
+  int C = 0, k = 0;
+};
+
 // Decode form of the block's FFN (bf16, few pairs per expert): every
 // workgroup lists its expert's pairs from the routing decisions topk_idx
 // [C][T*k] itself (no dispatch index pass); the intermediate rows and the
@@ -124,7 +139,8 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
 bool ffn_sel_ok(foe_dtype dt, int C, int E, int T, int k);
 hipError_t launch_expert_ffn_sel(int C, int E, int d, int F, int T, int k, const void* x,
                                  const int32_t* topk_idx, const void* w_gate, const void* w_up,
-                                 const void* w_down, void* y, void* scratch, hipStream_t s);
+                                 const void* w_down, void* y, void* scratch, hipStream_t s,
+                                 const FusedCombine& fc);
 // row_of_all == nullptr: y row of pair p of cluster h is h*T*k + p, skipped
 // when the expert id sel_all[h*T*k + p] is outside [0, E)
 hipError_t launch_combine_clusters(foe_dtype dt, int C, int T, int d, int k, const void* y,

@@ -125,7 +125,8 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
                                                         const float* __restrict__ bias, int T_,
                                                         int d, int E, int k,
                                                         int32_t* __restrict__ topk_idx,
-                                                        float* __restrict__ topk_w) {
+                                                        float* __restrict__ topk_w,
+                                                        int32_t* __restrict__ zcnt, int zn) {
   constexpr int UPW = (4 * TG + NW - 1) / NW;  // units per wave
   extern __shared__ __align__(16) unsigned char smem[];
   // cluster blockIdx.y: its router matrix, bias and output rows
@@ -136,6 +137,10 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
   const int t0 = blockIdx.x * kTok * TG;
+  // counters of later kernels of the same block call, per token of this tile
+  if (zcnt != nullptr && blockIdx.y == 0)
+    for (int i = threadIdx.x; i < kTok * TG * zn; i += NW * kWave)
+      if (t0 + i / zn < T_) zcnt[(size_t)t0 * zn + i] = 0;
 
   f32x4 acc[TG][NT];
 #pragma unroll
@@ -365,7 +370,8 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
 
 template <typename T, int NT, int NW, int TG, int KB = kBatch>
 hipError_t launch_nt(int C, int T_, int d, int E, int k, const void* x, const void* w,
-                     const float* bias, int32_t* idx, float* wt, hipStream_t s) {
+                     const float* bias, int32_t* idx, float* wt, hipStream_t s,
+                     int32_t* zcnt, int zn) {
   size_t lds_red = (size_t)NW * TG * NT * kWave * sizeof(f32x4);
   size_t lds_sel = (size_t)NW * 8 * k * 4;
   size_t lds = lds_red > lds_sel ? lds_red : lds_sel;
@@ -373,7 +379,7 @@ hipError_t launch_nt(int C, int T_, int d, int E, int k, const void* x, const vo
   ProfileScope ps("route", s);
   FOE_LAUNCH((route_kernel<T, NT, NW, TG, KB>), grid, dim3(NW * kWave), lds, s,
                      reinterpret_cast<const T*>(x), reinterpret_cast<const T*>(w), bias, T_, d,
-                     E, k, idx, wt);
+                     E, k, idx, wt, zcnt, zn);
   return hipGetLastError();
 }
 
@@ -417,11 +423,12 @@ hipError_t launch_stream(int C, int T_, int d, int E, int k, const void* x, cons
 
 template <typename T>
 hipError_t launch_t(int C, int T_, int d, int E, int k, const void* x, const void* w,
-                    const float* bias, int32_t* idx, float* wt, hipStream_t s) {
+                    const float* bias, int32_t* idx, float* wt, hipStream_t s, int32_t* zcnt,
+                    int zn) {
   const bool many = T_ >= 2048;
   if constexpr (sizeof(T) == 2) {
     // buffer offsets are 32-bit: x must span less than 2 GiB
-    if (FOE_ROUTE_STREAM && T_ >= FOE_ROUTE_STREAM_MIN_T && E <= 32 &&
+    if (FOE_ROUTE_STREAM && zcnt == nullptr && T_ >= FOE_ROUTE_STREAM_MIN_T && E <= 32 &&
         (size_t)T_ * d * 2 < ((size_t)1 << 31)) {
       // more waves per workgroup share each router row once there are enough
       // tokens for every CU
@@ -433,26 +440,30 @@ hipError_t launch_t(int C, int T_, int d, int E, int k, const void* x, const voi
   }
   if (E <= 16)
     return many ? launch_nt<T, 1, RouteCfg<FOE_ROUTE_TG16>::NW, RouteCfg<FOE_ROUTE_TG16>::TG>(
-                      C, T_, d, E, k, x, w, bias, idx, wt, s)
-                : launch_nt<T, 1, FOE_ROUTE_SMALL_NW, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
+                      C, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn)
+                : launch_nt<T, 1, FOE_ROUTE_SMALL_NW, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s,
+                                                          zcnt, zn);
   if (E <= 32)
     return many ? launch_nt<T, 2, RouteCfg<FOE_ROUTE_TG32>::NW, RouteCfg<FOE_ROUTE_TG32>::TG>(
-                      C, T_, d, E, k, x, w, bias, idx, wt, s)
-                : launch_nt<T, 2, FOE_ROUTE_SMALL_NW, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
-  if (E <= 64) return launch_nt<T, 4, 8, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
-  if (E <= 128) return launch_nt<T, 8, 4, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
-  return launch_nt<T, 16, 4, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s);
+                      C, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn)
+                : launch_nt<T, 2, FOE_ROUTE_SMALL_NW, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s,
+                                                          zcnt, zn);
+  if (E <= 64) return launch_nt<T, 4, 8, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
+  if (E <= 128) return launch_nt<T, 8, 4, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
+  return launch_nt<T, 16, 4, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
 }
 
 }  // namespace
 
 hipError_t launch_route(foe_dtype dt, int C, int T, int d, int E, int k, const void* x,
                         const void* w_router, const float* bias, int32_t* topk_idx,
-                        float* topk_w, hipStream_t s) {
+                        float* topk_w, hipStream_t s, int32_t* zero_cnt, int zero_per_tok) {
   if (T == 0 || C == 0) return hipSuccess;
   if (dt == FOE_BF16)
-    return launch_t<bf16>(C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s);
-  return launch_t<float>(C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s);
+    return launch_t<bf16>(C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s, zero_cnt,
+                          zero_per_tok);
+  return launch_t<float>(C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s, zero_cnt,
+                         zero_per_tok);
 }
 
 }  // namespace foe

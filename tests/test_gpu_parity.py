@@ -402,6 +402,32 @@ def test_block_is_deterministic():
     assert np.array_equal(a, b)
 
 
+def test_block_reused_workspace_new_inputs():
+    """Decode-sized block, two clusters, one workspace: first filled with 0xFF
+    bytes (garbage counters and rows), then used for input set A and then for
+    a different set B.  B must match the oracle, and match B run on a fresh
+    workspace bit for bit (no value of the earlier call leaks in)."""
+    say("block reused workspace")
+    outs = {}
+    base = dict(dtype="bf16", C=2, T=96, d=256, E=8, k=2, F=128, sigma=0.05, bias=None)
+    need = foe.workspace_bytes("cluster_block", foe.BF16, 2, 96, 256, 8, 2, 128)
+    ws = torch.full((need,), 255, dtype=torch.uint8, device=DEV)
+    for tag, seed in (("A", 11), ("B", 12)):
+        inp = synth.make_block_inputs(dict(base, seed=seed))
+        w = stacked(inp)
+        out = foe.cluster_block(to_dev(inp["x"], "bf16"), w["w_router"], w["bias"], w["w_gate"],
+                                w["w_up"], w["w_down"], 2, ws=ws)
+        torch.cuda.synchronize()
+        outs[tag] = (host(out), inp)
+    got, inp = outs["B"]
+    ref, res = oracle.cluster_block(inp["x"], inp["clusters"], 2, None)
+    exempt = np.zeros(96, dtype=bool)
+    for r in res:
+        exempt |= r["margin"] < EXEMPT
+    assert rel_err(got[~exempt], ref[~exempt]) <= TOL["bf16"]
+    assert np.array_equal(got, _block_gpu(inp))
+
+
 def test_pipeline_properties_at_prefill_size():
     """Properties that hold at any size, on the real prefill configuration:
     every permuted row holds its expert's token, segments ascend, the counts
