@@ -18,53 +18,22 @@
 // host sync is needed.
 //
 // bf16, few rows per expert (decode, weight-streaming bound): see
-// ffn_skinny_bf16.  fp32: plain FMA kernels (small shapes only).
+// ffn_stream_bf16.  fp32: plain FMA kernels (small shapes only).
 #include <type_traits>
 
 #include "lds_dma.hpp"
 
-// (BM, BN per weight matrix, waves along M, waves along N) of the large-M
-// kernel; (register staging sets, max waves per SIMD); (K-split waves, K
-// chunks per load batch) of the weight-streaming kernel.
-#ifndef FOE_PIPE_GU
-#define FOE_PIPE_GU 256, 128, 2, 4
-#endif
-#ifndef FOE_PIPE_DN
-#define FOE_PIPE_DN 256, 256, 2, 4
-#endif
-#ifndef FOE_PIPE_OPT
-#define FOE_PIPE_OPT 1, 2
-#endif
-#ifndef FOE_SKINNY
-#define FOE_SKINNY 2, 1
-#endif
-#ifndef FOE_SKINNY_PIPE
-#define FOE_SKINNY_PIPE 0
-#endif
-#ifndef FOE_SKINNY_ROT
-#define FOE_SKINNY_ROT 1
-#endif
-// LDS-DMA large-M kernel: on/off; (BM, BN, WM, WN, BK, LDS stages, waves that
-// issue the DMA (0 = all), M-tile group of the tile order, persistent)
-#ifndef FOE_GEMM_DMA
-#define FOE_GEMM_DMA 1
-#endif
+// LDS-DMA large-M kernel: (BM, BN, WM, WN, BK, LDS stages, waves that issue
+// the DMA (0 = all), M-tile group of the tile order, persistent)
 #ifndef FOE_DMA_GU
 #define FOE_DMA_GU 256, 128, 2, 4, 64, 2, 4, 4, 1
 #endif
 #ifndef FOE_DMA_DN
 #define FOE_DMA_DN 256, 256, 2, 4, 64, 2, 4, 4, 1
 #endif
-// few rows per expert (decode): the same kernel on 32-row tiles whose loads
-// cover 4 weight rows x 256 bytes each (the fastest HBM pattern measured),
-// or (FOE_DECODE_DMA 0) the register-streaming kernel
-#ifndef FOE_DECODE_DMA
-#define FOE_DECODE_DMA 0
-#endif
-// few rows per expert: per-wave LDS-staged weight stream (stages in flight)
-#ifndef FOE_DECODE_STREAM
-#define FOE_DECODE_STREAM 1
-#endif
+// few rows per expert (decode): LDS-staged weight stream with NS stages, K
+// walk rotated per workgroup, and (block decode form) pair lists built in the
+// kernel
 #ifndef FOE_FFN_SEL
 #define FOE_FFN_SEL 1
 #endif
@@ -73,12 +42,6 @@
 #endif
 #ifndef FOE_STREAM_NS
 #define FOE_STREAM_NS 3
-#endif
-#ifndef FOE_DMA_GU_DEC
-#define FOE_DMA_GU_DEC 32, 32, 1, 1, 128, 3, 1, 0, 0
-#endif
-#ifndef FOE_DMA_DN_DEC
-#define FOE_DMA_DN_DEC 32, 64, 1, 2, 128, 3, 1, 0, 0
 #endif
 
 namespace foe {
@@ -89,8 +52,6 @@ namespace {
 constexpr int kSelMax = 2048;
 constexpr int kScDevice = 16;  // buffer cache policy SC1: device-scope coherence
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-template <int W, int U> struct FirstOf { static constexpr int value = W; };
 
 // Find the (expert, first row, row end) of global M-tile `mt`.  Returns false
 // if `mt` is past the last tile.  Offsets are clamped to [0, rows]; a
@@ -177,240 +138,6 @@ __device__ __forceinline__ int src_row(const int32_t* __restrict__ gather, int k
   return (bid % kXcd) * per + bid / kXcd;
 }
 
-
-// Scheduling-group masks of __builtin_amdgcn_sched_group_barrier.
-constexpr int kSchedMfma = 0x008, kSchedDsRead = 0x100, kSchedDsWrite = 0x200,
-              kSchedVmemRead = 0x020;
-
-// Ask the scheduler for the order  MFMA, LDS read, <share of X>, MFMA, ...
-// over one k16 step: NM MFMAs, NR fragment reads and NX extra instructions of
-// kind XMASK spread evenly after the reads.  A wave issues in order, so a
-// burst of memory instructions would otherwise idle its MFMA pipe.
-template <int I, int NM, int NR, int NX, int XMASK>
-__device__ __forceinline__ void interleave() {
-  if constexpr (I < NM) {
-    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-    if constexpr (I < NR) {
-      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
-      constexpr int per = (NX + NR - 1) / NR;
-      constexpr int done = I * per;
-      constexpr int n = (NX - done) < per ? (NX - done) : per;
-      if constexpr (n > 0) __builtin_amdgcn_sched_group_barrier(XMASK, n, 0);
-    }
-    interleave<I + 1, NM, NR, NX, XMASK>();
-  }
-}
-
-template <int BM, int BN, int BK, int WM, int WN, bool GATEUP>
-struct GemmCfg {
-  static constexpr int NTHR = WM * WN * kWave;
-  static constexpr int WTM = BM / WM, WTN = BN / WN;
-  static constexpr int SM = WTM / 32, SN = WTN / 32;
-  static constexpr int NB = GATEUP ? 2 : 1;
-  static constexpr int LDK = BK + 8;  // padded LDS row (elements): conflict-free 16-byte reads
-  static constexpr int CPR = BK / 8;  // 16-byte chunks per tile row
-  static constexpr int A_PER = BM * CPR / NTHR;
-  static constexpr int B_PER = BN * CPR / NTHR;
-  static constexpr int A_ELEMS = BM * LDK, B_ELEMS = BN * LDK;
-  static constexpr int STAGE_ELEMS = A_ELEMS + NB * B_ELEMS;
-  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be a multiple of 32");
-  static_assert(BK % 16 == 0, "BK multiple of 16");
-  static_assert(BM * CPR % NTHR == 0 && BN * CPR % NTHR == 0, "even load split");
-};
-
-// Large-M grouped GEMM, BK = 64, two LDS stages.  Stage s is loaded into
-// register set s % NSETS and written to LDS one iteration before its MFMAs.
-// Per iteration (4 k16 steps):
-//   ks0: read frags ks1; MFMA ks0; write the staged next stage to the other
-//        LDS buffer
-//   ks1: read frags ks2; MFMA ks1; issue the global loads of a later stage
-//   ks2: read frags ks3; MFMA ks2; LDS barrier (next stage complete; nobody
-//        reads this stage's buffer any more)
-//   ks3: read frags ks0 of the next stage; MFMA ks3
-// With a gather list, operand row r of A is row gather[r]/kdiv of A.
-template <int BM, int BN, int WM, int WN, bool GATEUP, int NSETS, int MAXW>
-__global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1, MAXW)))
-void grouped_gemm_bf16(const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv,
-                       int a_rows, const int32_t* __restrict__ offsets, int E, int rows,
-                       const bf16* __restrict__ B0, const bf16* __restrict__ B1, int N, int K,
-                       bf16* __restrict__ out, int n_tiles_n, int n_tiles) {
-  constexpr int BK = 64;
-  using C = GemmCfg<BM, BN, BK, WM, WN, GATEUP>;
-  constexpr int NLD = C::A_PER + C::NB * C::B_PER;  // 16-byte loads per thread per stage
-  // two arrays so the compiler can tell the stages apart (the stage index is
-  // a compile-time constant in the unrolled loop)
-  __shared__ __align__(16) bf16 lds0[C::STAGE_ELEMS];
-  __shared__ __align__(16) bf16 lds1[C::STAGE_ELEMS];
-  auto stage = [&](int b) -> bf16* { return b ? lds1 : lds0; };
-
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  if (tile >= n_tiles) return;
-  const int mt = tile / n_tiles_n;
-  const int ntile = tile % n_tiles_n;
-  int e, row0, row_end;
-  if (!find_tile(offsets, E, rows, BM, mt, e, row0, row_end)) return;
-  const int n0 = ntile * BN;
-
-  const int tid = threadIdx.x;
-  const int lane = lane_id();
-  const int wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-
-  // A: a per-tile buffer (rows row0.. of a permuted copy) or, when gathering,
-  // the whole source with per-row offsets; weights: one buffer per slice
-  const int n_valid = min(BN, N - n0);
-  __amdgpu_buffer_rsrc_t rsrc[1 + C::NB];
-  if (gather == nullptr)
-    rsrc[0] = make_rsrc(A + (size_t)row0 * K, (uint32_t)min(BM, row_end - row0) * K * 2u);
-  else
-    rsrc[0] = make_rsrc(A, (uint32_t)a_rows * K * 2u);
-  rsrc[1] = make_rsrc(B0 + ((size_t)e * N + n0) * K, (uint32_t)n_valid * K * 2u);
-  if constexpr (GATEUP) rsrc[2] = make_rsrc(B1 + ((size_t)e * N + n0) * K, (uint32_t)n_valid * K * 2u);
-
-  // chunk i of a stage: byte offset in the K-slab (kOob for rows that read
-  // zeros), k of the chunk, LDS slot
-  uint32_t g_off[NLD];
-  int g_k[NLD], l_off[NLD];
-#pragma unroll
-  for (int i = 0; i < NLD; ++i) {
-    const bool is_a = i < C::A_PER;
-    const int j = is_a ? i : i - C::A_PER;
-    const int c = tid + (is_a ? j : j % C::B_PER) * C::NTHR;
-    const int r = c / C::CPR, kc = c % C::CPR;
-    g_k[i] = kc * 8;
-    if (is_a) {
-      l_off[i] = r * C::LDK + kc * 8;
-      if (gather == nullptr) {
-        g_off[i] = (uint32_t)(r * K + kc * 8) * 2u;
-      } else {
-        const int s = (row0 + r < row_end) ? src_row(gather, kdiv, row0 + r, a_rows) : -1;
-        g_off[i] = s < 0 ? kOob : ((uint32_t)s * K + kc * 8) * 2u;
-      }
-    } else {
-      l_off[i] = C::A_ELEMS + (j / C::B_PER) * C::B_ELEMS + r * C::LDK + kc * 8;
-      g_off[i] = (uint32_t)(r * K + kc * 8) * 2u;
-    }
-  }
-  auto rsrc_of = [&](int i) {
-    return i < C::A_PER ? rsrc[0] : rsrc[1 + (i - C::A_PER) / C::B_PER];
-  };
-
-  f32x16 acc[C::NB][C::SM][C::SN];
-#pragma unroll
-  for (int b = 0; b < C::NB; ++b)
-#pragma unroll
-    for (int i = 0; i < C::SM; ++i)
-#pragma unroll
-      for (int j = 0; j < C::SN; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[b][i][j][v] = 0.f;
-
-  u32x4 stg[NSETS][NLD];
-  auto gload = [&](int set, int k0) {
-    const uint32_t kb = (uint32_t)k0 * 2u;
-#pragma unroll
-    for (int i = 0; i < NLD; ++i)
-      stg[set][i] =
-          buf_load16(rsrc_of(i), (k0 + g_k[i] < K && g_off[i] != kOob) ? g_off[i] + kb : kOob);
-  };
-  auto lstore = [&](int set, int buf) {
-    bf16* sb = stage(buf);
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) *reinterpret_cast<u32x4*>(sb + l_off[i]) = stg[set][i];
-  };
-
-  const int lrow = lane & 31;
-  const int lk = (lane >> 5) * 8;
-  const int xa_base = (wm * C::WTM + lrow) * C::LDK + lk;
-  const int wf_base = C::A_ELEMS + (wn * C::WTN + lrow) * C::LDK + lk;
-  bf16x8 xa[2][C::SM];
-  bf16x8 wf[2][C::NB][C::SN];
-  auto fload = [&](int buf, int ks, int slot) {
-    const bf16* sa = stage(buf) + ks * 16;
-#pragma unroll
-    for (int i = 0; i < C::SM; ++i)
-      xa[slot][i] = *reinterpret_cast<const bf16x8*>(sa + xa_base + i * 32 * C::LDK);
-#pragma unroll
-    for (int b = 0; b < C::NB; ++b)
-#pragma unroll
-      for (int j = 0; j < C::SN; ++j)
-        wf[slot][b][j] =
-            *reinterpret_cast<const bf16x8*>(sa + wf_base + b * C::B_ELEMS + j * 32 * C::LDK);
-  };
-  auto mfma = [&](int slot) {
-#pragma unroll
-    for (int b = 0; b < C::NB; ++b)
-#pragma unroll
-      for (int j = 0; j < C::SN; ++j)
-#pragma unroll
-        for (int i = 0; i < C::SM; ++i)
-          acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[slot][b][j], xa[slot][i],
-                                                                 acc[b][i][j], 0, 0, 0);
-  };
-  constexpr int NM = C::NB * C::SM * C::SN;  // MFMAs per k16 step
-  constexpr int NR = C::SM + C::NB * C::SN;  // fragment reads per k16 step
-  // at iteration kt the register set of stage kt+1 is written to LDS and then
-  // refilled with stage kt+1+NSETS
-  auto iteration = [&](int kt, int cur) {
-    const int nxt = cur ^ 1;
-    const int set = (kt + 1) % NSETS;
-    fload(cur, 1, 1);
-    mfma(0);
-    lstore(set, nxt);
-    interleave<0, NM, NR, NLD, kSchedDsWrite>();
-    __builtin_amdgcn_sched_barrier(0);
-    fload(cur, 2, 0);
-    mfma(1);
-    gload(set, (kt + 1 + NSETS) * BK);
-    interleave<0, NM, NR, NLD, kSchedVmemRead>();
-    __builtin_amdgcn_sched_barrier(0);
-    fload(cur, 3, 1);
-    mfma(0);
-    interleave<0, NM, NR, 0, 0>();
-    __builtin_amdgcn_sched_barrier(0);
-    lds_barrier();
-    fload(nxt, 0, 0);
-    mfma(1);
-    interleave<0, NM, NR, 0, 0>();
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
-  // K steps rounded up to an even count: steps past K read zeros
-  const int nk = ((K + BK - 1) / BK + 1) & ~1;
-#pragma unroll
-  for (int st = 0; st < NSETS; ++st) gload(st, st * BK);
-  lstore(0, 0);
-  gload(0, NSETS * BK);
-  lds_barrier();
-  fload(0, 0, 0);
-  for (int kt = 0; kt < nk; kt += 2) {
-    iteration(kt, 0);
-    iteration(kt + 1, 1);
-  }
-
-  // epilogue: lane holds row m = .. + lane%32, columns n = .. + 8q + 4*(lane/32) + [0,4)
-#pragma unroll
-  for (int i = 0; i < C::SM; ++i) {
-    const int m = row0 + wm * C::WTM + i * 32 + lrow;
-    if (m >= row_end) continue;
-#pragma unroll
-    for (int j = 0; j < C::SN; ++j) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int n = n0 + wn * C::WTN + j * 32 + q * 8 + (lane >> 5) * 4;
-        if (n >= N) continue;
-        bf16x4 o;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          float val = acc[0][i][j][q * 4 + v];
-          if constexpr (GATEUP) val = silu_f(val) * acc[C::NB - 1][i][j][q * 4 + v];
-          o[v] = (bf16)val;
-        }
-        *reinterpret_cast<bf16x4*>(out + (size_t)m * N + n) = o;
-      }
-    }
-  }
-}
 
 // ---- LDS-DMA variant of the large-M grouped GEMM ---------------------------
 // Operand tiles go from global memory straight into LDS with
@@ -750,148 +477,6 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
   }
 }
 
-// Few rows per expert (decode): the FFN is a weight stream.  A workgroup owns
-// one expert and a slice of weight rows (16 gate + 16 up rows, or 32 down
-// rows); its KW waves split K and read the weights with 128-bit buffer loads
-// straight into the operands of v_mfma_f32_16x16x32_bf16 (D = W * A^T, 16
-// weight rows x 16 rows of A per MFMA), so there is no LDS staging and each
-// wave has U K chunks of loads in flight.  The KW partial tiles are summed in
-// LDS in wave order.  Experts with more than 32 rows take several passes.
-template <bool GATEUP, int KW, int U>
-__global__ __launch_bounds__(KW * 64) void ffn_skinny_bf16(
-    const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv, int a_rows,
-    const int32_t* __restrict__ offsets, int E, int rows, const bf16* __restrict__ W0,
-    const bf16* __restrict__ W1, int N, int K, bf16* __restrict__ out, int n_groups) {
-  constexpr int NPB = GATEUP ? 16 : 32;  // output columns per workgroup
-  __shared__ __align__(16) f32x4 red[KW][2][2][kWave];
-
-  const int e = blockIdx.x / n_groups;
-  const int n0 = (blockIdx.x % n_groups) * NPB;
-  const int a = min(max(offsets[e], 0), rows);
-  const int b = max(min(max(offsets[e + 1], 0), rows), a);
-  if (b == a || e >= E) return;
-  const int lane = lane_id();
-  const int wave = threadIdx.x >> 6;
-  const int r16 = lane & 15;
-  const uint32_t kq = (uint32_t)(lane >> 4) * 8u;
-
-  // weight tiles: tile 0 / tile 1 = gate / up rows n0.. (GATEUP) or rows n0.., n0+16..
-  const int nv = min(NPB, N - n0);
-  const __amdgpu_buffer_rsrc_t wr0 =
-      make_rsrc(W0 + ((size_t)e * N + n0) * K, (uint32_t)nv * K * 2u);
-  const __amdgpu_buffer_rsrc_t wr1 =
-      GATEUP ? make_rsrc(W1 + ((size_t)e * N + n0) * K, (uint32_t)nv * K * 2u) : wr0;
-  const uint32_t w_off0 = (uint32_t)r16 * K * 2u + kq * 2u;
-  const uint32_t w_off1 = GATEUP ? w_off0 : (uint32_t)(r16 + 16) * K * 2u + kq * 2u;
-  const __amdgpu_buffer_rsrc_t ar = make_rsrc(A, (uint32_t)a_rows * K * 2u);
-  const int nchunks = (K + 31) / 32;
-  const int k_rot = (int)((blockIdx.x * 37u) % (unsigned)nchunks) / (KW * U) * (KW * U);
-
-  for (int t0 = a; t0 < b; t0 += 32) {
-    const int tv = min(32, b - t0);
-    uint32_t a_off[2];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int t = j * 16 + r16;
-      const int s = t < tv ? src_row(gather, kdiv, t0 + t, a_rows) : -1;
-      a_off[j] = s < 0 ? kOob : (uint32_t)s * K * 2u + kq * 2u;
-    }
-    f32x4 acc[2][2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // batches of U chunks, two register sets: the loads of the next batch are
-    // in flight while the MFMAs of the current one run
-    u32x4 wa[2][U][2], xb[2][U][2];
-    auto load = [&](int set, int c0) {
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        int c = c0 + u;
-        // workgroups start their K walk at different chunks, so that at any
-        // moment they read different column ranges of their weight rows
-        if constexpr (FOE_SKINNY_ROT) c = c < nchunks ? (c + k_rot) % nchunks : c;
-        const bool ok = c < nchunks && (uint32_t)c * 32u + kq < (uint32_t)K;
-        const uint32_t kb = (uint32_t)c * 64u;
-        wa[set][u][0] = buf_load16_stream(wr0, ok ? w_off0 + kb : kOob);
-        wa[set][u][1] = buf_load16_stream(wr1, ok ? w_off1 + kb : kOob);
-        xb[set][u][0] = buf_load16(ar, (ok && a_off[0] != kOob) ? a_off[0] + kb : kOob);
-        xb[set][u][1] = buf_load16(ar, (ok && a_off[1] != kOob) ? a_off[1] + kb : kOob);
-      }
-    };
-    auto compute = [&](int set) {
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, wa[set][u][i]), __builtin_bit_cast(bf16x8, xb[set][u][j]),
-                acc[i][j], 0, 0, 0);
-    };
-    constexpr int STEP = KW * U;
-    if constexpr (FOE_SKINNY_PIPE) {
-      int c0 = wave * U;
-      if (c0 < nchunks) load(0, c0);
-      for (; c0 < nchunks; c0 += 2 * STEP) {
-        if (c0 + STEP < nchunks) load(1, c0 + STEP);
-        compute(0);
-        if (c0 + STEP >= nchunks) break;
-        if (c0 + 2 * STEP < nchunks) load(0, c0 + 2 * STEP);
-        compute(1);
-      }
-    } else {
-      for (int c0 = wave * U; c0 < nchunks; c0 += STEP) {
-        load(0, c0);
-        compute(0);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) red[wave][i][j][lane] = acc[i][j];
-    __syncthreads();
-    if (wave == 0) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          f32x4 s4 = red[0][i][j][lane];
-#pragma unroll
-          for (int w = 1; w < KW; ++w) s4 += red[w][i][j][lane];
-          acc[i][j] = s4;
-        }
-      // lane holds row j*16 + lane%16 of A and weight rows 4*(lane/16) + [0,4)
-      const int nb = 4 * (lane >> 4);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int t = j * 16 + r16;
-        if (t >= tv) continue;
-        bf16* orow = out + (size_t)(t0 + t) * N + n0;
-        if constexpr (GATEUP) {
-          if (nb < nv) {
-            bf16x4 o;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) o[v] = (bf16)(silu_f(acc[0][j][v]) * acc[1][j][v]);
-            *reinterpret_cast<bf16x4*>(orow + nb) = o;
-          }
-        } else {
-#pragma unroll
-          for (int i = 0; i < 2; ++i) {
-            if (i * 16 + nb >= nv) continue;
-            bf16x4 o;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) o[v] = (bf16)acc[i][j][v];
-            *reinterpret_cast<bf16x4*>(orow + i * 16 + nb) = o;
-          }
-        }
-      }
-    }
-    __syncthreads();
-  }
-}
-
 // Few rows per expert (decode), LDS-staged weight stream.  A workgroup of 4
 // waves takes one expert and 4 consecutive weight tiles (each 16 gate + 16 up
 // rows, or 32 down rows), one per wave, over all of K, for up to 32 rows of A
@@ -1002,7 +587,7 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
     // the wave counts give the positions.  The weight DMAs stay in flight.
     if (nks >= NS - 1) vm_wait<8 * (NS - 1)>();
     else vm_wait<0>();
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    lds_barrier();
     const int* sel = reinterpret_cast<const int*>(smem + NS * SB);
     int* lw = reinterpret_cast<int*>(smem + NS * SB + SELB);
     int* wc = lw + kSelMax;
@@ -1013,7 +598,7 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
       const bool ok = f < r_sel && sel[f] == le;
       const uint64_t m = __ballot(ok);
       if (lane == 0) wc[wave] = __popcll(m);
-      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      lds_barrier();
       int pre = 0, tot = 0;
 #pragma unroll
       for (int w = 0; w < WPB; ++w) {
@@ -1023,7 +608,7 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
       }
       if (ok) lw[n + pre + __popcll(m & below)] = f;
       n += tot;
-      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      lds_barrier();
     }
     b = n;
   } else {
@@ -1108,7 +693,7 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
       if (kt + NS - 2 >= nks) vm_wait<0>();
       else if (u < NS - 1 && kt == u) vm_wait<2 * (NS - 2 - u) + NI * u>();
       else vm_wait<NI * (NS - 2)>();
-      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      lds_barrier();
       if (kt + NS - 1 < nks) {
         issue_w(kt + NS - 1, s_next);
         issue_x(kt + NS - 1, s_next);
@@ -1227,8 +812,6 @@ __global__ __launch_bounds__(256) void ffn_stream_bf16(
   }
 }
 
-constexpr int kSkinnyWaves = FirstOf<FOE_SKINNY>::value;
-
 
 // ---- fp32 path: plain FMA kernels (small shapes) ---------------------------
 __device__ int expert_of_row(const int32_t* __restrict__ offsets, int E, int rows, int row) {
@@ -1279,20 +862,6 @@ __global__ __launch_bounds__(256) void down_f32(const float* __restrict__ h,
   float acc = 0.f;
   for (int i = 0; i < F; ++i) acc = fmaf(hr[i], w[i], acc);
   y[(size_t)row * d + c] = acc;
-}
-
-template <int BM, int BN, int WM, int WN, bool GATEUP, int NSETS, int MAXW>
-void launch_gemm(const bf16* A, const int32_t* gather, int kdiv, int a_rows,
-                 const int32_t* offsets, int E, int rows, const bf16* B0, const bf16* B1, int N,
-                 int K, bf16* out, hipStream_t s, const char* name) {
-  const int ntn = ceil_div(N, BN);
-  const int max_mt = ceil_div(rows, BM) + E;  // sum_e ceil(M_e/BM) <= rows/BM + E
-  const long long n_tiles = (long long)max_mt * ntn;
-  dim3 grid((unsigned)((n_tiles + 7) / 8 * 8));
-  ProfileScope ps(name, s);
-  FOE_LAUNCH((grouped_gemm_bf16<BM, BN, WM, WN, GATEUP, NSETS, MAXW>), grid,
-                     dim3(WM * WN * kWave), 0, s, A, gather, kdiv, a_rows, offsets, E, rows, B0,
-                     B1, N, K, out, ntn, (int)n_tiles);
 }
 
 // compute units of the current device (one persistent workgroup each)
@@ -1365,63 +934,34 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
   const bf16* wd = reinterpret_cast<const bf16*>(w_down);
   bf16* h = reinterpret_cast<bf16*>(scratch);
   bf16* y = reinterpret_cast<bf16*>(y_perm);
-  if (rows < 64 * E && FOE_DECODE_STREAM) {  // few rows per expert: weight-streaming bound
+  if (rows < 64 * E) {  // few rows per expert: weight-streaming bound
     {
       const int ng = ceil_div(F, 16);
       ProfileScope ps("ffn_gateup", s);
       FOE_LAUNCH((ffn_stream_bf16<true, FOE_STREAM_NS, false>), dim3(E * ceil_div(ng, 4)),
-                         dim3(256), 0, s, xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F,
-                         d, h, ng, 1, 0, FusedCombine{});
+                 dim3(256), 0, s, xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F, d, h,
+                 ng, 1, 0, FusedCombine{});
     }
     {
       const int ng = ceil_div(d, 32);
       ProfileScope ps("ffn_down", s);
-      FOE_LAUNCH((ffn_stream_bf16<false, FOE_STREAM_NS, false>),
-                         dim3(E * ceil_div(ng, 4)), dim3(256), 0, s, static_cast<const bf16*>(h),
-                         nullptr, 1, rows, offsets, E, rows, wd, nullptr, d, F, y, ng, 1, 0,
-                         FusedCombine{});
-    }
-  } else if (rows < 64 * E && FOE_DECODE_DMA) {
-    DmaLaunch<FOE_DMA_GU_DEC>::run<true>(xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F, d,
-                                         h, s, "ffn_gateup");
-    DmaLaunch<FOE_DMA_DN_DEC>::run<false>(static_cast<const bf16*>(h), (const int32_t*)nullptr, 1,
-                                          rows, offsets, E, rows, wd, (const bf16*)nullptr, d, F,
-                                          y, s, "ffn_down");
-  } else if (rows < 64 * E) {
-    {
-      const int ng = ceil_div(F, 16);
-      ProfileScope ps("ffn_gateup", s);
-      FOE_LAUNCH((ffn_skinny_bf16<true, FOE_SKINNY>), dim3(E * ng),
-                         dim3(kSkinnyWaves * kWave), 0, s, xa, gather, kdiv, a_rows, offsets, E,
-                         rows, wg, wu, F, d, h, ng);
-    }
-    {
-      const int ng = ceil_div(d, 32);
-      ProfileScope ps("ffn_down", s);
-      FOE_LAUNCH((ffn_skinny_bf16<false, FOE_SKINNY>), dim3(E * ng),
-                         dim3(kSkinnyWaves * kWave), 0, s, h, nullptr, 1, rows, offsets, E, rows,
-                         wd, nullptr, d, F, y, ng);
+      FOE_LAUNCH((ffn_stream_bf16<false, FOE_STREAM_NS, false>), dim3(E * ceil_div(ng, 4)),
+                 dim3(256), 0, s, static_cast<const bf16*>(h), nullptr, 1, rows, offsets, E,
+                 rows, wd, nullptr, d, F, y, ng, 1, 0, FusedCombine{});
     }
   } else {
-#if FOE_GEMM_DMA
     DmaLaunch<FOE_DMA_GU>::run<true>(xa, gather, kdiv, a_rows, offsets, E, rows, wg, wu, F, d, h,
                                      s, "ffn_gateup");
     DmaLaunch<FOE_DMA_DN>::run<false>(static_cast<const bf16*>(h), (const int32_t*)nullptr, 1,
                                       rows, offsets, E, rows, wd, (const bf16*)nullptr, d, F, y, s,
                                       "ffn_down");
-#else
-    launch_gemm<FOE_PIPE_GU, true, FOE_PIPE_OPT>(xa, gather, kdiv, a_rows, offsets, E, rows, wg,
-                                                 wu, F, d, h, s, "ffn_gateup");
-    launch_gemm<FOE_PIPE_DN, false, FOE_PIPE_OPT>(h, nullptr, 1, rows, offsets, E, rows, wd,
-                                                  nullptr, d, F, y, s, "ffn_down");
-#endif
   }
   return hipGetLastError();
 }
 
 bool ffn_sel_ok(foe_dtype dt, int C, int E, int T, int k) {
   const long long R = (long long)T * k;
-  return FOE_FFN_SEL && FOE_DECODE_STREAM && dt == FOE_BF16 && R > 0 && R <= kSelMax &&
+  return FOE_FFN_SEL && dt == FOE_BF16 && R > 0 && R <= kSelMax &&
          (long long)C * R < 64LL * C * E;
 }
 

@@ -7,27 +7,15 @@
 
 namespace foe {
 
-// Buffer resource over `nbytes` bytes from `base`: loads at offsets at or past
-// `nbytes` return zeros, which handles ragged rows and K tails without branches.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t nbytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nbytes, 0x00020000);
-}
-__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
-}
-// weight stream of the decode kernel: read once per call (cache policy AUX)
-#ifndef FOE_WSTREAM_AUX
-#define FOE_WSTREAM_AUX 0
-#endif
-__device__ __forceinline__ u32x4 buf_load16_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, FOE_WSTREAM_AUX));
-}
-constexpr uint32_t kOob = 0x80000000u;  // past every buffer range used here: reads zeros
+// Buffer resources end where the valid rows / K end: loads at offsets at or
+// past the range return zeros, which handles ragged rows and K tails without
+// branches.  kOob lies past every range used here.
+constexpr uint32_t kOob = 0x80000000u;
 
 // LDS-only workgroup barrier: waits for this wave's LDS operations and meets
 // the other waves, but (unlike __syncthreads) does not drain outstanding
 // global loads, so prefetches stay in flight across it.
-[[maybe_unused]] __device__ __forceinline__ void lds_barrier() {
+__device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
@@ -56,8 +44,8 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, u
                "s"(r), "s"(lds), "i"(imm)
                : "memory");
 }
-// wait until at most N of this wave's global loads are outstanding and its
-// LDS reads are done, then meet the other waves
+// wait until at most N of this wave's vector memory operations are
+// outstanding and its LDS operations are done, then meet the other waves
 template <int N>
 __device__ __forceinline__ void vm_barrier() {
   asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
@@ -74,7 +62,8 @@ __device__ __forceinline__ int swz(int r) {
   else return ((r >> 1) & 3) ^ ((r >> 3) & 1);
 }
 
-// wait until at most N of this wave's global loads are outstanding
+// wait until at most N of this wave's vector memory operations are outstanding
+// (loads retire in issue order)
 template <int N>
 __device__ __forceinline__ void vm_wait() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");

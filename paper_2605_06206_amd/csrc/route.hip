@@ -294,7 +294,7 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
   auto body = [&](int kt, int s, int s_next) {
     if (kt + NS - 2 < nks) vm_wait<NI * (NS - 2)>();
     else vm_wait<0>();
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    lds_barrier();
     if (kt + NS - 1 < nks) issue(kt + NS - 1, s_next);
     const unsigned char* src = smem + s * SB + rbase;
 #pragma unroll
