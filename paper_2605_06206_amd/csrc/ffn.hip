@@ -53,6 +53,21 @@ constexpr int kSelMax = 2048;
 constexpr int kScDevice = 16;  // buffer cache policy SC1: device-scope coherence
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
+// Number of M-tiles of BM rows over all experts (segments clamped as in
+// find_tile); every lane of the wave gets the total.
+__device__ int total_mtiles(const int32_t* __restrict__ offsets, int E, int rows, int BM) {
+  const int lane = lane_id();
+  int mine = 0;
+  for (int e = lane; e < E; e += kWave) {
+    const int a = min(max(offsets[e], 0), rows);
+    const int b = min(max(offsets[e + 1], 0), rows);
+    mine += b > a ? (b - a + BM - 1) / BM : 0;
+  }
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) mine += __shfl_xor(mine, off);
+  return mine;
+}
+
 // Find the (expert, first row, row end) of global M-tile `mt`.  Returns false
 // if `mt` is past the last tile.  Offsets are clamped to [0, rows]; a
 // decreasing bound gives an empty segment.  Lane l counts the tiles of a
@@ -440,6 +455,10 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
     }
   };
 
+  // M-tiles that hold rows (persistent form: the tile list is split over
+  // the XCDs by this count, not by the launch's upper bound)
+  const int m_tiles = PERSIST ? __builtin_amdgcn_readfirstlane(total_mtiles(offsets, E, rows, BM))
+                              : n_tiles / n_tiles_n;
   // tile t -> (M-tile, N-tile): groups of GM M-tiles are walked N-tile by
   // N-tile, so that a run of consecutive tiles shares A rows and weight slices
   auto tile_coords = [&](int t, int& mt, int& nt) {
@@ -449,7 +468,7 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
     } else {
       // the last group may hold fewer than GM M-tiles
       const int grp = t / (GM * n_tiles_n), i = t % (GM * n_tiles_n);
-      const int g = min(GM, n_tiles / n_tiles_n - grp * GM);
+      const int g = min(GM, m_tiles - grp * GM);
       mt = grp * GM + i % g;
       nt = i / g;
     }
@@ -459,8 +478,9 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
     // rounds, so the tiles that share operands run side by side
     constexpr int kXcd = 8;
     const int x = blockIdx.x % kXcd, l = blockIdx.x / kXcd, nl = gridDim.x / kXcd;
-    const int per = (n_tiles + kXcd - 1) / kXcd;
-    for (int q = l; q < per && x * per + q < n_tiles; q += nl) {
+    const int n_real = m_tiles * n_tiles_n;
+    const int per = (n_real + kXcd - 1) / kXcd;
+    for (int q = l; q < per && x * per + q < n_real; q += nl) {
       int mt, nt, e, row0, row_end;
       tile_coords(x * per + q, mt, nt);
       if (!find_tile(offsets, E, rows, BM, mt, e, row0, row_end)) continue;
