@@ -143,17 +143,6 @@ __device__ __forceinline__ int src_row(const int32_t* __restrict__ gather, int k
   return s < src_rows ? s : -1;
 }
 
-// Workgroups are dealt round-robin to the 8 XCDs (each with its own L2).  The
-// tile index is remapped so that each XCD walks a contiguous range of tiles:
-// neighbouring tiles share their A rows (same M-tile) or their weight slice
-// (same expert), and now meet in the same L2.
-[[maybe_unused]] __device__ __forceinline__ int xcd_tile(int bid, int nblocks) {
-  constexpr int kXcd = 8;
-  const int per = (nblocks + kXcd - 1) / kXcd;
-  return (bid % kXcd) * per + bid / kXcd;
-}
-
-
 // ---- LDS-DMA variant of the large-M grouped GEMM ---------------------------
 // Operand tiles go from global memory straight into LDS with
 // `buffer_load_dwordx4 ... lds`: each lane of a wave deposits 16 bytes at
@@ -474,21 +463,21 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
     }
   };
   if constexpr (PERSIST) {
-    // one workgroup per CU; the workgroups of an XCD take its tile range in
-    // rounds, so the tiles that share operands run side by side
-    constexpr int kXcd = 8;
-    const int x = blockIdx.x % kXcd, l = blockIdx.x / kXcd, nl = gridDim.x / kXcd;
+    // one workgroup per CU, tiles dealt round-robin: the tiles running at any
+    // moment are a window of consecutive tiles of the order above, spread
+    // over all XCDs, and their shared A rows and weight slices meet in the
+    // Infinity Cache that every XCD reads through (measured faster than
+    // giving each XCD a contiguous range for its own L2)
     const int n_real = m_tiles * n_tiles_n;
-    const int per = (n_real + kXcd - 1) / kXcd;
-    for (int q = l; q < per && x * per + q < n_real; q += nl) {
+    for (int t = blockIdx.x; t < n_real; t += gridDim.x) {
       int mt, nt, e, row0, row_end;
-      tile_coords(x * per + q, mt, nt);
+      tile_coords(t, mt, nt);
       if (!find_tile(offsets, E, rows, BM, mt, e, row0, row_end)) continue;
       vm_barrier<0>();  // the previous tile's LDS reads are done everywhere
       run_tile(e, row0, row_end, nt);
     }
   } else {
-    const int tile = xcd_tile(blockIdx.x, gridDim.x);
+    const int tile = blockIdx.x;
     if (tile >= n_tiles) return;
     int mt, nt, e, row0, row_end;
     tile_coords(tile, mt, nt);
