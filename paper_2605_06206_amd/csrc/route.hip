@@ -123,13 +123,16 @@ template <typename T, int NT, int NW, int TG, int KB>
 __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
                                                         const T* __restrict__ w,
                                                         const float* __restrict__ bias, int T_,
-                                                        int d, int E, int k,
+                                                        int d, int E, int k, int G,
                                                         int32_t* __restrict__ topk_idx,
                                                         float* __restrict__ topk_w,
                                                         int32_t* __restrict__ zcnt, int zn) {
   constexpr int UPW = (4 * TG + NW - 1) / NW;  // units per wave
   extern __shared__ __align__(16) unsigned char smem[];
-  // cluster blockIdx.y: its router matrix, bias and output rows
+  // cluster blockIdx.y: its router matrix, bias and output rows.  With G > 1
+  // groups in one workgroup, the G router matrices [G][E][d] are one score
+  // matrix of G*E columns and each group's top-k is taken over its own block
+  // of E columns (the output of group h goes to topk_*[h][T][k]).
   w += (size_t)blockIdx.y * E * d;
   if (bias != nullptr) bias += (size_t)blockIdx.y * E;
   topk_idx += (size_t)blockIdx.y * T_ * k;
@@ -147,7 +150,8 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
   for (int g = 0; g < TG; ++g)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[g][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  RouteMma<T>::template run<NT, NW, TG, KB>(x, w, T_, d, E, t0, wave, lane, acc);
+  const int Et = G * E;  // score columns
+  RouteMma<T>::template run<NT, NW, TG, KB>(x, w, T_, d, Et, t0, wave, lane, acc);
 
   // partial tiles of the NW waves -> LDS [wave][g][nt][lane] (f32x4)
   f32x4* part = reinterpret_cast<f32x4*>(smem);
@@ -171,7 +175,7 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
 #pragma unroll
         for (int wv = 0; wv < NW; ++wv) s += part[((wv * TG + g) * NT + nt) * kWave + lane][i];
         const int e = nt * 16 + col;
-        if (bias != nullptr && e < E) s += bias[e];
+        if (bias != nullptr && e < Et) s += bias[e];
       }
       gl[u][nt] = s;
     }
@@ -187,38 +191,44 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
     const int unit = wave + u * NW;
     if (unit >= 4 * TG) break;
     const int tok = t0 + (unit >> 2) * 16 + 4 * row + (unit & 3);
-    unsigned taken = 0;  // bit nt: expert nt*16 + col already selected / absent
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      if (nt * 16 + col >= E) taken |= 1u << nt;
-    for (int s = 0; s < k; ++s) {
-      float bv = -__builtin_inff();
-      int be = 0x7fffffff;
+    for (int h = 0; h < G; ++h) {
+      // bit nt: column nt*16 + col outside group h or already selected
+      unsigned taken = 0;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         const int e = nt * 16 + col;
-        if (!((taken >> nt) & 1u) && beats(gl[u][nt], e, bv, be)) { bv = gl[u][nt]; be = e; }
+        if (e < h * E || e >= (h + 1) * E) taken |= 1u << nt;
       }
-      argmax_step<8>(bv, be);
-      argmax_step<4>(bv, be);
-      argmax_step<2>(bv, be);
-      argmax_step<1>(bv, be);
-      if (be != 0x7fffffff && (be & 15) == col) taken |= 1u << (be >> 4);
-      if (col == 0) {
-        sel_e[row * k + s] = (be == 0x7fffffff) ? -1 : be;
-        sel_v[row * k + s] = bv;
+      for (int s = 0; s < k; ++s) {
+        float bv = -__builtin_inff();
+        int be = 0x7fffffff;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int e = nt * 16 + col;
+          if (!((taken >> nt) & 1u) && beats(gl[u][nt], e, bv, be)) { bv = gl[u][nt]; be = e; }
+        }
+        argmax_step<8>(bv, be);
+        argmax_step<4>(bv, be);
+        argmax_step<2>(bv, be);
+        argmax_step<1>(bv, be);
+        if (be != 0x7fffffff && (be & 15) == col) taken |= 1u << (be >> 4);
+        if (col == 0) {
+          sel_e[row * k + s] = (be == 0x7fffffff) ? -1 : be - h * E;
+          sel_v[row * k + s] = bv;
+        }
       }
-    }
-    // softmax over the selected scores (this wave's own rows; LDS operations
-    // of one wave complete in order); lane col writes slots col, col+16, ...
-    if (tok < T_) {
-      const float m = sel_v[row * k];
-      float z = 0.f;
-      for (int s = 0; s < k; ++s) z += expf(sel_v[row * k + s] - m);
-      const float inv = 1.0f / z;
-      for (int s = col; s < k; s += 16) {
-        topk_idx[(size_t)tok * k + s] = sel_e[row * k + s];
-        topk_w[(size_t)tok * k + s] = expf(sel_v[row * k + s] - m) * inv;
+      // softmax over the selected scores (this wave's own rows; LDS operations
+      // of one wave complete in order); lane col writes slots col, col+16, ...
+      if (tok < T_) {
+        const float m = sel_v[row * k];
+        float z = 0.f;
+        for (int s = 0; s < k; ++s) z += expf(sel_v[row * k + s] - m);
+        const float inv = 1.0f / z;
+        const size_t o = ((size_t)h * T_ + tok) * k;
+        for (int s = col; s < k; s += 16) {
+          topk_idx[o + s] = sel_e[row * k + s];
+          topk_w[o + s] = expf(sel_v[row * k + s] - m) * inv;
+        }
       }
     }
   }
@@ -368,18 +378,19 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
   }
 }
 
+// C clusters as G groups of every workgroup (G = C) or one per grid row (G = 1)
 template <typename T, int NT, int NW, int TG, int KB = kBatch>
-hipError_t launch_nt(int C, int T_, int d, int E, int k, const void* x, const void* w,
+hipError_t launch_nt(int C, int G, int T_, int d, int E, int k, const void* x, const void* w,
                      const float* bias, int32_t* idx, float* wt, hipStream_t s,
                      int32_t* zcnt, int zn) {
   size_t lds_red = (size_t)NW * TG * NT * kWave * sizeof(f32x4);
   size_t lds_sel = (size_t)NW * 8 * k * 4;
   size_t lds = lds_red > lds_sel ? lds_red : lds_sel;
-  dim3 grid(ceil_div(T_, kTok * TG), C);
+  dim3 grid(ceil_div(T_, kTok * TG), C / G);
   ProfileScope ps("route", s);
   FOE_LAUNCH((route_kernel<T, NT, NW, TG, KB>), grid, dim3(NW * kWave), lds, s,
-                     reinterpret_cast<const T*>(x), reinterpret_cast<const T*>(w), bias, T_, d,
-                     E, k, idx, wt, zcnt, zn);
+             reinterpret_cast<const T*>(x), reinterpret_cast<const T*>(w), bias, T_, d, E, k, G,
+             idx, wt, zcnt, zn);
   return hipGetLastError();
 }
 
@@ -405,6 +416,9 @@ template <int TG_, int NW_> struct RouteCfg {
 #ifndef FOE_ROUTE_TG32
 #define FOE_ROUTE_TG32 2, 8
 #endif
+#ifndef FOE_ROUTE_TG64
+#define FOE_ROUTE_TG64 1, 8
+#endif
 template <int WPB>
 hipError_t launch_stream(int C, int T_, int d, int E, int k, const void* x, const void* w,
                          const float* bias, int32_t* idx, float* wt, hipStream_t s) {
@@ -426,10 +440,14 @@ hipError_t launch_t(int C, int T_, int d, int E, int k, const void* x, const voi
                     const float* bias, int32_t* idx, float* wt, hipStream_t s, int32_t* zcnt,
                     int zn) {
   const bool many = T_ >= 2048;
+  // several clusters: one pass over x scores all C*E experts (the router
+  // matrices are contiguous) and each cluster takes its top-k from its block
+  const int G = (C > 1 && C * E <= 256) ? C : 1;
+  const int Et = G * E;
   if constexpr (sizeof(T) == 2) {
     // buffer offsets are 32-bit: x must span less than 2 GiB
-    if (FOE_ROUTE_STREAM && zcnt == nullptr && T_ >= FOE_ROUTE_STREAM_MIN_T && E <= 32 &&
-        (size_t)T_ * d * 2 < ((size_t)1 << 31)) {
+    if (FOE_ROUTE_STREAM && G == 1 && zcnt == nullptr && T_ >= FOE_ROUTE_STREAM_MIN_T &&
+        E <= 32 && (size_t)T_ * d * 2 < ((size_t)1 << 31)) {
       // more waves per workgroup share each router row once there are enough
       // tokens for every CU
       ProfileScope ps("route", s);
@@ -438,19 +456,22 @@ hipError_t launch_t(int C, int T_, int d, int E, int k, const void* x, const voi
       return launch_stream<2>(C, T_, d, E, k, x, w, bias, idx, wt, s);
     }
   }
-  if (E <= 16)
+  if (Et <= 16)
     return many ? launch_nt<T, 1, RouteCfg<FOE_ROUTE_TG16>::NW, RouteCfg<FOE_ROUTE_TG16>::TG>(
-                      C, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn)
-                : launch_nt<T, 1, FOE_ROUTE_SMALL_NW, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s,
-                                                          zcnt, zn);
-  if (E <= 32)
+                      C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn)
+                : launch_nt<T, 1, FOE_ROUTE_SMALL_NW, 1>(C, G, T_, d, E, k, x, w, bias, idx, wt,
+                                                          s, zcnt, zn);
+  if (Et <= 32)
     return many ? launch_nt<T, 2, RouteCfg<FOE_ROUTE_TG32>::NW, RouteCfg<FOE_ROUTE_TG32>::TG>(
-                      C, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn)
-                : launch_nt<T, 2, FOE_ROUTE_SMALL_NW, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s,
-                                                          zcnt, zn);
-  if (E <= 64) return launch_nt<T, 4, 8, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
-  if (E <= 128) return launch_nt<T, 8, 4, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
-  return launch_nt<T, 16, 4, 1>(C, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
+                      C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn)
+                : launch_nt<T, 2, FOE_ROUTE_SMALL_NW, 1>(C, G, T_, d, E, k, x, w, bias, idx, wt,
+                                                          s, zcnt, zn);
+  if (Et <= 64)
+    return many ? launch_nt<T, 4, RouteCfg<FOE_ROUTE_TG64>::NW, RouteCfg<FOE_ROUTE_TG64>::TG>(
+                      C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn)
+                : launch_nt<T, 4, 8, 1>(C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
+  if (Et <= 128) return launch_nt<T, 8, 4, 1>(C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
+  return launch_nt<T, 16, 4, 1>(C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
 }
 
 }  // namespace
