@@ -381,6 +381,8 @@ def test_block_parity_sampled(name):
     (200, 64, 100, 3, 64, 3, None, "bf16", None),    # 300 experts in one grouped FFN
     (600, 128, 64, 2, 128, 4, None, "bf16", None),    # 256 experts, large-tile path
     (5000, 64, 8, 2, 64, 2, None, "bf16", None),      # two clusters, multi-block dispatch
+    (40, 136, 6, 2, 200, 2, None, "bf16", None),      # decode form, d and F off the tile widths
+    (70, 64, 10, 3, 64, 3, None, "bf16", "zipf1.2"),  # cluster blocks straddle 16-column tiles
 ])
 def test_block_parity_shapes(T, d, E, k, F, C, scale, dt, bias):
     say("block shapes", T, d, E, k, F, C, scale, dt, bias)
