@@ -61,6 +61,19 @@ typedef enum {
 typedef enum { FOE_F32 = 0, FOE_BF16 = 1 } foe_dtype;
 
 /*
+ * Routing weights of the selected experts (Section 3.1 routing equation; the
+ * paper leaves renormalisation open):
+ *   FOE_GATE_RENORM  softmax over the k selected scores of the group: the
+ *                    global softmax renormalised over the selection (each
+ *                    token's k weights of a group sum to 1)
+ *   FOE_GATE_GLOBAL  the global softmax over the single score vector of all
+ *                    C*E experts (all groups), taken at the selected experts
+ *                    and not renormalised (OLMoE-style gating; each group's
+ *                    weights sum to its share of the probability mass)
+ */
+typedef enum { FOE_GATE_RENORM = 0, FOE_GATE_GLOBAL = 1 } foe_gating;
+
+/*
  * foe_route - router scores, per-group top-k and routing weights.
  * Section 3.1, routing equation: g[i] = Router(r_full[i]) and
  * I_h[i], w_h[i] = TopK over the group's experts of g[i].
@@ -79,6 +92,19 @@ typedef enum { FOE_F32 = 0, FOE_BF16 = 1 } foe_dtype;
 int foe_route(foe_dtype dt, int T, int d, int E, int k,
               const void* x, const void* w_router, const float* bias,
               int32_t* topk_idx, float* topk_w, void* stream);
+
+/*
+ * foe_route_ex - foe_route for G groups sharing x, with a gating choice.
+ * The G router matrices w_router [G,E,d] (and bias [G,E] or NULL) form one
+ * score vector of G*E experts per token; group h takes its top-k over its own
+ * block of E scores and writes topk_idx/topk_w [G,T,k] rows h*T.. (ids local
+ * to the group, 0..E-1).  gating: FOE_GATE_RENORM (foe_route's weights) or
+ * FOE_GATE_GLOBAL (softmax over all G*E scores, not renormalised).
+ * FOE_ERR_UNSUPPORTED when G*E > 256 with G > 1.  Needs no workspace.
+ */
+int foe_route_ex(foe_dtype dt, int G, int T, int d, int E, int k, foe_gating gating,
+                 const void* x, const void* w_router, const float* bias,
+                 int32_t* topk_idx, float* topk_w, void* stream);
 
 /*
  * foe_permute - expert histogram, prefix sum and stable token permutation:
@@ -165,12 +191,16 @@ int foe_reduce(foe_dtype dt, int C, int T, int d,
  * update" rows), followed by the local reduction:
  *   out = reduce_scale * sum_h (x + delta_h),
  *   delta_h[i] = sum_{e in I_h[i]} w_h[i,e] FFN_{h,e}(x[i]).
- * Routing runs per cluster; the dispatch of all clusters is numbered in one
- * pass, one grouped FFN covers all C*E experts and reads the rows of x through
- * the permutation (no permuted copy of x is written), and one kernel forms
- * every cluster's weighted sum and the reduction (no per-cluster partial is
- * written).  Evaluated as reduce_scale * (C * x + S) with S the fp32 sum of
- * the weighted expert rows in the order (h = 0..C-1, j = 0..k-1).
+ * One routing pass scores all clusters (one read of x when C*E <= 256) and
+ * each cluster takes its top-k over its own experts; the dispatch of all
+ * clusters is numbered in one pass (at decode sizes each FFN workgroup lists
+ * its expert's pairs itself); one grouped FFN covers all C*E experts and
+ * reads the rows of x through the permutation (no permuted copy of x is
+ * written); the weighted sums of every cluster and the reduction are formed
+ * in one pass (at decode sizes inside the down-projection kernel) and no
+ * per-cluster partial is written.  Evaluated as reduce_scale * (C * x + S)
+ * with S the fp32 sum of the weighted expert rows in the order
+ * (h = 0..C-1, j = 0..k-1).  Weights are FOE_GATE_RENORM.
  *
  *   x         [T,d]       dt
  *   w_router  [C,E,d]     dt;   bias [C,E] fp32 or NULL
@@ -188,6 +218,18 @@ int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F,
                       void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * foe_cluster_block_ex - foe_cluster_block with a gating choice (see
+ * foe_gating).  FOE_GATE_GLOBAL normalises over all C*E scores of a token and
+ * is supported for C == 1 or C*E <= 256 (else FOE_ERR_UNSUPPORTED).  Same
+ * workspace as foe_cluster_block.
+ */
+int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
+                         foe_gating gating, const void* x, const void* w_router,
+                         const float* bias, const void* w_gate, const void* w_up,
+                         const void* w_down, float reduce_scale, void* out,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/*
  * foe_workspace_bytes - workspace size in bytes for `op` (host string:
  * "route", "permute", "expert_ffn", "combine", "reduce", "cluster_block").
  * Arguments an op does not use are ignored (pass 0); for "expert_ffn" T is the
@@ -202,8 +244,9 @@ const char* foe_last_error(void);
 
 /*
  * Kernel timing (for measurement).  While enabled, every kernel the library
- * enqueues is bracketed by two HIP events recorded on the same stream; the
- * records accumulate until foe_profile_reset().  Reading waits on the events.
+ * enqueues carries two HIP events that its dispatch stamps at its start and
+ * end (on the same stream); the records accumulate until foe_profile_reset().
+ * Reading waits on the events.
  *   foe_profile_enable(1/0)          start / stop recording (returns FOE_OK)
  *   foe_profile_reset()              drop all records
  *   foe_profile_kernel(name, &n, &ms)  launches and summed milliseconds of the

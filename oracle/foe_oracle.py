@@ -21,7 +21,9 @@ Readings where the paper is silent (each is listed in the design doc):
 * the router is a linear map ``W_r [E,d]`` with an optional bias ``[E]``;
 * selection is decided on fp32 scores, descending, equal scores -> lower id;
 * the weights are the softmax over the selected scores (global softmax
-  renormalised over the top-k; the partition function cancels);
+  renormalised over the top-k; the partition function cancels); the other
+  reading, the global softmax over all groups' scores without
+  renormalisation, is ``gate_weights_global``;
 * ``FFN_e`` is SwiGLU without biases: ``W_d (silu(W_g x) * (W_u x))``;
 * dropless: every (token, slot) pair is processed;
 * dispatch order is (expert ascending, token ascending) = stable counting sort.
@@ -38,6 +40,7 @@ __all__ = [
     "router_logits",
     "topk_select",
     "gate_weights",
+    "gate_weights_global",
     "route",
     "expert_histogram",
     "permutation",
@@ -112,6 +115,27 @@ def gate_weights(logits, idx):
     gsel = np.take_along_axis(_f64(logits), np.asarray(idx), axis=1)
     z = np.exp(gsel - gsel.max(axis=1, keepdims=True))
     return z / z.sum(axis=1, keepdims=True)
+
+
+def gate_weights_global(group_logits, group_idx):
+    """Routing weights with the global softmax of Section 3.1, not renormalised.
+
+    The paper's routers give one score vector per token over the experts of
+    all groups; here the G groups' score blocks ``group_logits[h]`` [T,E]
+    together form that vector.  The weight of a selected expert ``e`` of group
+    ``h`` is its probability under the softmax of the whole vector:
+    ``exp(g_h[i,e] - m_i) / sum_{h',e'} exp(g_h'[i,e'] - m_i)`` with ``m_i``
+    the largest score of token ``i`` over all groups (any ``m_i`` gives the same
+    value; it only keeps ``exp`` in range).  fp64.  Returns one [T,k] array per
+    group.
+    """
+    gl = [_f64(g) for g in group_logits]
+    m = np.max(np.stack([g.max(axis=1) for g in gl]), axis=0)[:, None]
+    z = np.zeros_like(m)
+    for g in gl:
+        z = z + np.exp(g - m).sum(axis=1, keepdims=True)
+    return [np.exp(np.take_along_axis(g, np.asarray(ix), axis=1) - m) / z
+            for g, ix in zip(gl, group_idx)]
 
 
 def route(x, w_router, bias, k):
@@ -224,15 +248,18 @@ def reduce_partials(partials, scale, residual=None):
     return scale * acc
 
 
-def cluster_delta(x, cl, k):
+def cluster_delta(x, cl, k, r=None):
     """One cluster's pipeline: route, histogram, permute, grouped FFN, combine.
 
     ``cl`` holds ``w_router`` [E,d], ``bias`` [E] or None, ``w_gate``/``w_up``
-    [E,F,d], ``w_down`` [E,d,F].  Returns a dict with every intermediate and
-    ``delta`` = the MoE sum of Table 3 without the residual.
+    [E,F,d], ``w_down`` [E,d,F].  ``r`` is the cluster's routing (a ``route``
+    dict, possibly with other weights) or None to route here.  Returns a dict
+    with every intermediate and ``delta`` = the MoE sum of Table 3 without the
+    residual.
     """
     E = np.asarray(cl["w_router"]).shape[0]
-    r = route(x, cl["w_router"], cl.get("bias"), k)
+    if r is None:
+        r = route(x, cl["w_router"], cl.get("bias"), k)
     counts, offsets = expert_histogram(r["idx"], E)
     sorted_src, row_of = permutation(r["idx"])
     x_perm = gather_rows(x, sorted_src, k)
@@ -243,17 +270,26 @@ def cluster_delta(x, cl, k):
     return r
 
 
-def cluster_block(x, clusters, k, reduce_scale=None):
+def cluster_block(x, clusters, k, reduce_scale=None, gating="renorm"):
     """C co-resident clusters sharing the input ``x`` (the paper's ``r_full``).
 
     ``P_h = x + delta_h`` is the group partial ``x'[h]`` of Table 3 and
     ``out = reduce_scale * sum_h P_h`` (default ``1/C``, the average).
+    ``gating`` = "renorm" (``gate_weights``) or "global"
+    (``gate_weights_global`` over all clusters' scores).
     Returns ``(out, per_cluster_results)``.
     """
     C = len(clusters)
     if reduce_scale is None:
         reduce_scale = 1.0 / C
-    res = [cluster_delta(x, cl, k) for cl in clusters]
+    routes = [route(x, cl["w_router"], cl.get("bias"), k) for cl in clusters]
+    if gating == "global":
+        ws = gate_weights_global([r["logits"] for r in routes], [r["idx"] for r in routes])
+        for r, w in zip(routes, ws):
+            r["w"] = w
+    elif gating != "renorm":
+        raise ValueError("gating must be 'renorm' or 'global'")
+    res = [cluster_delta(x, cl, k, r) for cl, r in zip(clusters, routes)]
     partials = np.stack([r["delta"] for r in res])
     return reduce_partials(partials, reduce_scale, residual=x), res
 

@@ -189,6 +189,32 @@ size_t foe_workspace_bytes(const char* op, foe_dtype dt, int C, int T, int d, in
   return SIZE_MAX;
 }
 
+int foe_route_ex(foe_dtype dt, int G, int T, int d, int E, int k, foe_gating gating,
+                 const void* x, const void* w_router, const float* bias, int32_t* topk_idx,
+                 float* topk_w, void* stream) {
+  Check c;
+  check_dtype(c, dt);
+  c.need(G >= 1 && G <= 64, "G must be in [1, 64]");
+  check_route_shape(c, T, E, k);
+  c.need((long long)G * T * (k < 1 ? 1 : k) <= INT_MAX, "G*T*k must fit in int32");
+  check_dim8(c, d, "d must be a positive multiple of 8");
+  c.need(gating == FOE_GATE_RENORM || gating == FOE_GATE_GLOBAL,
+         "gating must be FOE_GATE_RENORM or FOE_GATE_GLOBAL");
+  const bool any = T > 0;
+  c.tensor(x, any, "x");
+  c.tensor(w_router, any, "w_router");
+  c.small(bias, false, "bias");
+  c.small(topk_idx, any, "topk_idx");
+  c.small(topk_w, any, "topk_w");
+  if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_route_ex: " + c.err);
+  if (!route_one_pass(G, E))
+    return fail(FOE_ERR_UNSUPPORTED, "foe_route_ex: G > 1 needs G*E <= 256");
+  hipError_t e = launch_route(dt, G, T, d, E, k, gating, x, w_router, bias, topk_idx, topk_w,
+                              reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "foe_route_ex");
+  return FOE_OK;
+}
+
 int foe_route(foe_dtype dt, int T, int d, int E, int k, const void* x, const void* w_router,
               const float* bias, int32_t* topk_idx, float* topk_w, void* stream) {
   Check c;
@@ -202,8 +228,8 @@ int foe_route(foe_dtype dt, int T, int d, int E, int k, const void* x, const voi
   c.small(topk_idx, any, "topk_idx");
   c.small(topk_w, any, "topk_w");
   if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_route: " + c.err);
-  hipError_t e = launch_route(dt, 1, T, d, E, k, x, w_router, bias, topk_idx, topk_w,
-                              reinterpret_cast<hipStream_t>(stream));
+  hipError_t e = launch_route(dt, 1, T, d, E, k, FOE_GATE_RENORM, x, w_router, bias, topk_idx,
+                              topk_w, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "foe_route");
   return FOE_OK;
 }
@@ -311,7 +337,18 @@ int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F, co
                       const void* w_router, const float* bias, const void* w_gate,
                       const void* w_up, const void* w_down, float reduce_scale, void* out,
                       void* ws, size_t ws_bytes, void* stream) {
+  return foe_cluster_block_ex(dt, C, T, d, E, k, F, FOE_GATE_RENORM, x, w_router, bias, w_gate,
+                              w_up, w_down, reduce_scale, out, ws, ws_bytes, stream);
+}
+
+int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
+                         foe_gating gating, const void* x, const void* w_router,
+                         const float* bias, const void* w_gate, const void* w_up,
+                         const void* w_down, float reduce_scale, void* out, void* ws,
+                         size_t ws_bytes, void* stream) {
   Check c;
+  c.need(gating == FOE_GATE_RENORM || gating == FOE_GATE_GLOBAL,
+         "gating must be FOE_GATE_RENORM or FOE_GATE_GLOBAL");
   check_dtype(c, dt);
   c.need(C >= 1 && C <= 64, "C must be in [1, 64]");
   check_route_shape(c, T, E, k);
@@ -327,6 +364,9 @@ int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F, co
   c.tensor(w_down, any, "w_down");
   c.tensor(out, any, "out");
   if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_cluster_block: " + c.err);
+  if (gating == FOE_GATE_GLOBAL && !route_one_pass(C, E))
+    return fail(FOE_ERR_UNSUPPORTED,
+                "foe_cluster_block: global gating needs C == 1 or C*E <= 256");
   if (!any) return FOE_OK;
   const long long CR = (long long)C * T * k;
   if (dt == FOE_BF16 && !(operand_fits(T, d, 2) && operand_fits(CR, F, 2) && operand_fits(CR, d, 2)))
@@ -355,7 +395,7 @@ int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F, co
   // 1. routing of every cluster in one grid (Section 3.1: one score vector,
   //    per-group top-k)
   const bool sel = ffn_sel_ok(dt, C, E, T, k);
-  hipError_t e = launch_route(dt, C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s,
+  hipError_t e = launch_route(dt, C, T, d, E, k, gating, x, w_router, bias, topk_idx, topk_w, s,
                               sel ? reinterpret_cast<int32_t*>(base + L.cnt) : nullptr,
                               ceil_div(d, 128));
   if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/route");

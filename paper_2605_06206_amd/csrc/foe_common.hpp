@@ -90,10 +90,14 @@ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 // ---- kernel launchers (one translation unit each) -------------------------
 // C clusters in one grid: w_router [C][E][d], bias [C][E], outputs [C][T][k].
 // zero_cnt != nullptr: the kernel also clears zero_cnt[T][zero_per_tok].
-hipError_t launch_route(foe_dtype dt, int C, int T, int d, int E, int k, const void* x,
-                        const void* w_router, const float* bias, int32_t* topk_idx,
-                        float* topk_w, hipStream_t s, int32_t* zero_cnt = nullptr,
-                        int zero_per_tok = 0);
+// gating: FOE_GATE_RENORM or FOE_GATE_GLOBAL (the global softmax needs every
+// cluster's scores in one workgroup: C == 1 or C*E <= 256).
+hipError_t launch_route(foe_dtype dt, int C, int T, int d, int E, int k, int gating,
+                        const void* x, const void* w_router, const float* bias,
+                        int32_t* topk_idx, float* topk_w, hipStream_t s,
+                        int32_t* zero_cnt = nullptr, int zero_per_tok = 0);
+// whether all C clusters' scores of a token are formed in one workgroup
+inline bool route_one_pass(int C, int E) { return C == 1 || C * E <= 256; }
 
 // permute scratch = 2 * C * nblk * E int32 (see permute_blocks())
 int permute_blocks(int R);

@@ -32,6 +32,33 @@ __device__ __forceinline__ void argmax_step(float& bv, int& be) {
   if (beats(ov, oe, bv, be)) { bv = ov; be = oe; }
 }
 
+// Global softmax normaliser of one token whose score columns nt*16 + col (col
+// = lane % 16) sit in the lanes of a 16-lane row: the row maximum m and
+// z = sum over the valid columns (< ncol) of exp(g - m), both in every lane
+// of the row (rotation reductions, a fixed order).
+template <int NT>
+__device__ __forceinline__ void row_softmax_norm(const float (&g)[NT], int col, int ncol,
+                                                 float& m, float& z) {
+  float mx = -__builtin_inff();
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+    if (nt * 16 + col < ncol) mx = fmaxf(mx, g[nt]);
+  mx = fmaxf(mx, __int_as_float(row_ror<8>(__float_as_int(mx))));
+  mx = fmaxf(mx, __int_as_float(row_ror<4>(__float_as_int(mx))));
+  mx = fmaxf(mx, __int_as_float(row_ror<2>(__float_as_int(mx))));
+  mx = fmaxf(mx, __int_as_float(row_ror<1>(__float_as_int(mx))));
+  float sm = 0.f;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+    if (nt * 16 + col < ncol) sm += expf(g[nt] - mx);
+  sm += __int_as_float(row_ror<8>(__float_as_int(sm)));
+  sm += __int_as_float(row_ror<4>(__float_as_int(sm)));
+  sm += __int_as_float(row_ror<2>(__float_as_int(sm)));
+  sm += __int_as_float(row_ror<1>(__float_as_int(sm)));
+  m = mx;
+  z = sm;
+}
+
 template <typename T> struct RouteMma;
 
 // bf16: each MFMA step consumes 32 k; lane (r = l%16, q = l/16) supplies
@@ -123,7 +150,7 @@ template <typename T, int NT, int NW, int TG, int KB>
 __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
                                                         const T* __restrict__ w,
                                                         const float* __restrict__ bias, int T_,
-                                                        int d, int E, int k, int G,
+                                                        int d, int E, int k, int G, int gating,
                                                         int32_t* __restrict__ topk_idx,
                                                         float* __restrict__ topk_w,
                                                         int32_t* __restrict__ zcnt, int zn) {
@@ -191,6 +218,10 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
     const int unit = wave + u * NW;
     if (unit >= 4 * TG) break;
     const int tok = t0 + (unit >> 2) * 16 + 4 * row + (unit & 3);
+    // global gating: softmax over all G*E scores of the token, not
+    // renormalised over the selection
+    float gm = 0.f, gz = 1.f;
+    if (gating == FOE_GATE_GLOBAL) row_softmax_norm<NT>(gl[u], col, Et, gm, gz);
     for (int h = 0; h < G; ++h) {
       // bit nt: column nt*16 + col outside group h or already selected
       unsigned taken = 0;
@@ -220,9 +251,12 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
       // softmax over the selected scores (this wave's own rows; LDS operations
       // of one wave complete in order); lane col writes slots col, col+16, ...
       if (tok < T_) {
-        const float m = sel_v[row * k];
-        float z = 0.f;
-        for (int s = 0; s < k; ++s) z += expf(sel_v[row * k + s] - m);
+        float m = gm, z = gz;
+        if (gating != FOE_GATE_GLOBAL) {
+          m = sel_v[row * k];
+          z = 0.f;
+          for (int s = 0; s < k; ++s) z += expf(sel_v[row * k + s] - m);
+        }
         const float inv = 1.0f / z;
         const size_t o = ((size_t)h * T_ + tok) * k;
         for (int s = col; s < k; s += 16) {
@@ -243,7 +277,8 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
 template <int NT, int NS, int WPB>
 __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
     const bf16* __restrict__ x, const bf16* __restrict__ w, const float* __restrict__ bias,
-    int T_, int d, int E, int k, int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
+    int T_, int d, int E, int k, int gating, int32_t* __restrict__ topk_idx,
+    float* __restrict__ topk_w) {
   constexpr int XB = WPB * 4096;          // token rows of a stage (16 rows x 256 B per wave)
   constexpr int SB = XB + NT * 4096;      // + router rows (16 rows x 256 B per expert tile)
   constexpr int WI = NT * 4 / WPB;        // router instructions per wave and stage
@@ -343,6 +378,8 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
       gl[nt] = acc[nt][i] + ((bias != nullptr && e < E) ? bias[e] : 0.f);
     }
     const int tok = t0 + 4 * row + i;
+    float gm = 0.f, gz = 1.f;  // global gating: softmax over all E scores
+    if (gating == FOE_GATE_GLOBAL) row_softmax_norm<NT>(gl, col, E, gm, gz);
     unsigned taken = 0;  // bit nt: expert nt*16 + col already selected / absent
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
@@ -366,9 +403,12 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
       }
     }
     if (tok < T_) {
-      const float m = sel_v[row * k];
-      float z = 0.f;
-      for (int s = 0; s < k; ++s) z += expf(sel_v[row * k + s] - m);
+      float m = gm, z = gz;
+      if (gating != FOE_GATE_GLOBAL) {
+        m = sel_v[row * k];
+        z = 0.f;
+        for (int s = 0; s < k; ++s) z += expf(sel_v[row * k + s] - m);
+      }
       const float inv = 1.0f / z;
       for (int s = col; s < k; s += 16) {
         topk_idx[(size_t)tok * k + s] = sel_e[row * k + s];
@@ -380,8 +420,8 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
 
 // C clusters as G groups of every workgroup (G = C) or one per grid row (G = 1)
 template <typename T, int NT, int NW, int TG, int KB = kBatch>
-hipError_t launch_nt(int C, int G, int T_, int d, int E, int k, const void* x, const void* w,
-                     const float* bias, int32_t* idx, float* wt, hipStream_t s,
+hipError_t launch_nt(int C, int G, int T_, int d, int E, int k, int gating, const void* x,
+                     const void* w, const float* bias, int32_t* idx, float* wt, hipStream_t s,
                      int32_t* zcnt, int zn) {
   size_t lds_red = (size_t)NW * TG * NT * kWave * sizeof(f32x4);
   size_t lds_sel = (size_t)NW * 8 * k * 4;
@@ -390,7 +430,7 @@ hipError_t launch_nt(int C, int G, int T_, int d, int E, int k, const void* x, c
   ProfileScope ps("route", s);
   FOE_LAUNCH((route_kernel<T, NT, NW, TG, KB>), grid, dim3(NW * kWave), lds, s,
              reinterpret_cast<const T*>(x), reinterpret_cast<const T*>(w), bias, T_, d, E, k, G,
-             idx, wt, zcnt, zn);
+             gating, idx, wt, zcnt, zn);
   return hipGetLastError();
 }
 
@@ -420,23 +460,24 @@ template <int TG_, int NW_> struct RouteCfg {
 #define FOE_ROUTE_TG64 1, 8
 #endif
 template <int WPB>
-hipError_t launch_stream(int C, int T_, int d, int E, int k, const void* x, const void* w,
-                         const float* bias, int32_t* idx, float* wt, hipStream_t s) {
+hipError_t launch_stream(int C, int T_, int d, int E, int k, int gating, const void* x,
+                         const void* w, const float* bias, int32_t* idx, float* wt,
+                         hipStream_t s) {
   constexpr int NS = 4;
   dim3 grid(ceil_div(T_, 16 * WPB), C);
   const bf16* xb = reinterpret_cast<const bf16*>(x);
   const bf16* wb = reinterpret_cast<const bf16*>(w);
   if (E <= 16)
     FOE_LAUNCH((route_stream_kernel<1, NS, WPB>), grid, dim3(WPB * kWave), 0, s, xb, wb,
-                       bias, T_, d, E, k, idx, wt);
+                       bias, T_, d, E, k, gating, idx, wt);
   else
     FOE_LAUNCH((route_stream_kernel<2, NS, WPB>), grid, dim3(WPB * kWave), 0, s, xb, wb,
-                       bias, T_, d, E, k, idx, wt);
+                       bias, T_, d, E, k, gating, idx, wt);
   return hipGetLastError();
 }
 
 template <typename T>
-hipError_t launch_t(int C, int T_, int d, int E, int k, const void* x, const void* w,
+hipError_t launch_t(int C, int T_, int d, int E, int k, int gating, const void* x, const void* w,
                     const float* bias, int32_t* idx, float* wt, hipStream_t s, int32_t* zcnt,
                     int zn) {
   const bool many = T_ >= 2048;
@@ -452,39 +493,42 @@ hipError_t launch_t(int C, int T_, int d, int E, int k, const void* x, const voi
       // tokens for every CU
       ProfileScope ps("route", s);
       if (T_ >= 16384)
-        return launch_stream<4>(C, T_, d, E, k, x, w, bias, idx, wt, s);
-      return launch_stream<2>(C, T_, d, E, k, x, w, bias, idx, wt, s);
+        return launch_stream<4>(C, T_, d, E, k, gating, x, w, bias, idx, wt, s);
+      return launch_stream<2>(C, T_, d, E, k, gating, x, w, bias, idx, wt, s);
     }
   }
   if (Et <= 16)
     return many ? launch_nt<T, 1, RouteCfg<FOE_ROUTE_TG16>::NW, RouteCfg<FOE_ROUTE_TG16>::TG>(
-                      C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn)
-                : launch_nt<T, 1, FOE_ROUTE_SMALL_NW, 1>(C, G, T_, d, E, k, x, w, bias, idx, wt,
-                                                          s, zcnt, zn);
+                      C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn)
+                : launch_nt<T, 1, FOE_ROUTE_SMALL_NW, 1>(C, G, T_, d, E, k, gating, x, w, bias,
+                                                          idx, wt, s, zcnt, zn);
   if (Et <= 32)
     return many ? launch_nt<T, 2, RouteCfg<FOE_ROUTE_TG32>::NW, RouteCfg<FOE_ROUTE_TG32>::TG>(
-                      C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn)
-                : launch_nt<T, 2, FOE_ROUTE_SMALL_NW, 1>(C, G, T_, d, E, k, x, w, bias, idx, wt,
-                                                          s, zcnt, zn);
+                      C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn)
+                : launch_nt<T, 2, FOE_ROUTE_SMALL_NW, 1>(C, G, T_, d, E, k, gating, x, w, bias,
+                                                          idx, wt, s, zcnt, zn);
   if (Et <= 64)
     return many ? launch_nt<T, 4, RouteCfg<FOE_ROUTE_TG64>::NW, RouteCfg<FOE_ROUTE_TG64>::TG>(
-                      C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn)
-                : launch_nt<T, 4, 8, 1>(C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
-  if (Et <= 128) return launch_nt<T, 8, 4, 1>(C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
-  return launch_nt<T, 16, 4, 1>(C, G, T_, d, E, k, x, w, bias, idx, wt, s, zcnt, zn);
+                      C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn)
+                : launch_nt<T, 4, 8, 1>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt,
+                                        zn);
+  if (Et <= 128)
+    return launch_nt<T, 8, 4, 1>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn);
+  return launch_nt<T, 16, 4, 1>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn);
 }
 
 }  // namespace
 
-hipError_t launch_route(foe_dtype dt, int C, int T, int d, int E, int k, const void* x,
-                        const void* w_router, const float* bias, int32_t* topk_idx,
-                        float* topk_w, hipStream_t s, int32_t* zero_cnt, int zero_per_tok) {
+hipError_t launch_route(foe_dtype dt, int C, int T, int d, int E, int k, int gating,
+                        const void* x, const void* w_router, const float* bias,
+                        int32_t* topk_idx, float* topk_w, hipStream_t s, int32_t* zero_cnt,
+                        int zero_per_tok) {
   if (T == 0 || C == 0) return hipSuccess;
   if (dt == FOE_BF16)
-    return launch_t<bf16>(C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s, zero_cnt,
-                          zero_per_tok);
-  return launch_t<float>(C, T, d, E, k, x, w_router, bias, topk_idx, topk_w, s, zero_cnt,
-                         zero_per_tok);
+    return launch_t<bf16>(C, T, d, E, k, gating, x, w_router, bias, topk_idx, topk_w, s,
+                          zero_cnt, zero_per_tok);
+  return launch_t<float>(C, T, d, E, k, gating, x, w_router, bias, topk_idx, topk_w, s,
+                         zero_cnt, zero_per_tok);
 }
 
 }  // namespace foe

@@ -16,6 +16,8 @@ import torch
 
 F32 = 0
 BF16 = 1
+GATE_RENORM = 0   # foe_gating
+GATE_GLOBAL = 1
 
 FOE_OK = 0
 FOE_ERR_INVALID = -1
@@ -30,6 +32,8 @@ _p = ctypes.c_void_p
 
 _SIGNATURES = {
     "foe_route": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _p, _p, _p, _p, _p, _p]),
+    "foe_route_ex": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _p, _p, _p,
+                              _p, _p, _p]),
     "foe_permute": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _p, _p, _p, _p, _p, _p, _p,
                              _p, _c_size, _p]),
     "foe_expert_ffn": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _p, _p, _p, _p, _p, _p,
@@ -38,6 +42,9 @@ _SIGNATURES = {
     "foe_reduce": (_c_int, [_c_int, _c_int, _c_int, _c_int, _p, _p, _c_float, _p, _p]),
     "foe_cluster_block": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _p, _p,
                                    _p, _p, _p, _p, _c_float, _p, _p, _c_size, _p]),
+    "foe_cluster_block_ex": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                      _c_int, _p, _p, _p, _p, _p, _p, _c_float, _p, _p, _c_size,
+                                      _p]),
     "foe_workspace_bytes": (_c_size, [ctypes.c_char_p, _c_int, _c_int, _c_int, _c_int, _c_int,
                                       _c_int, _c_int]),
     "foe_last_error": (ctypes.c_char_p, []),
@@ -123,19 +130,33 @@ def _workspace(ws, nbytes, device):
     return ws
 
 
-def route(x, w_router, bias, k, topk_idx=None, topk_w=None, stream=None):
-    """foe_route: returns (topk_idx [T,k] int32, topk_w [T,k] fp32)."""
+def _gating(gating):
+    codes = {"renorm": GATE_RENORM, "global": GATE_GLOBAL}
+    if gating not in codes:
+        raise ValueError(f"gating must be 'renorm' or 'global', got {gating!r}")
+    return codes[gating]
+
+
+def route(x, w_router, bias, k, topk_idx=None, topk_w=None, stream=None, gating="renorm"):
+    """foe_route (w_router [E,d]) or foe_route_ex (w_router [G,E,d], or a
+    gating other than "renorm"): returns (topk_idx, topk_w), [T,k] or [G,T,k]."""
     T, d = x.shape
-    E = w_router.shape[0]
+    grouped = w_router.dim() == 3
+    G = w_router.shape[0] if grouped else 1
+    E = w_router.shape[-2]
     dt = _dt(x)
+    shape = (G, T, k) if grouped else (T, k)
     if topk_idx is None:
-        topk_idx = torch.empty((T, k), dtype=torch.int32, device=x.device)
+        topk_idx = torch.empty(shape, dtype=torch.int32, device=x.device)
     if topk_w is None:
-        topk_w = torch.empty((T, k), dtype=torch.float32, device=x.device)
-    rc = lib().foe_route(dt, T, d, E, k, _dev(x, "x"), _dev(w_router, "w_router", x.dtype),
-                         _dev(bias, "bias", torch.float32), _dev(topk_idx, "topk_idx", torch.int32),
-                         _dev(topk_w, "topk_w", torch.float32), _stream(stream))
-    _check(rc, "foe_route")
+        topk_w = torch.empty(shape, dtype=torch.float32, device=x.device)
+    args = (_dev(x, "x"), _dev(w_router, "w_router", x.dtype), _dev(bias, "bias", torch.float32),
+            _dev(topk_idx, "topk_idx", torch.int32), _dev(topk_w, "topk_w", torch.float32),
+            _stream(stream))
+    if not grouped and gating == "renorm":
+        _check(lib().foe_route(dt, T, d, E, k, *args), "foe_route")
+    else:
+        _check(lib().foe_route_ex(dt, G, T, d, E, k, _gating(gating), *args), "foe_route_ex")
     return topk_idx, topk_w
 
 
@@ -212,8 +233,9 @@ def reduce(partials, scale, residual=None, out=None, stream=None):
 
 
 def cluster_block(x, w_router, bias, w_gate, w_up, w_down, k, reduce_scale=None, out=None,
-                  ws=None, stream=None):
-    """foe_cluster_block for C clusters: weights stacked on a leading C axis."""
+                  ws=None, stream=None, gating="renorm"):
+    """foe_cluster_block (foe_cluster_block_ex for a gating other than "renorm")
+    for C clusters: weights stacked on a leading C axis."""
     T, d = x.shape
     C, E, F, _ = w_gate.shape
     dt = _dt(x)
@@ -223,14 +245,15 @@ def cluster_block(x, w_router, bias, w_gate, w_up, w_down, k, reduce_scale=None,
         out = torch.empty((T, d), dtype=x.dtype, device=x.device)
     need = workspace_bytes("cluster_block", dt, C, T, d, E, k, F)
     ws = _workspace(ws, need, x.device)
-    rc = lib().foe_cluster_block(dt, C, T, d, E, k, F, _dev(x, "x"),
-                                 _dev(w_router, "w_router", x.dtype),
-                                 _dev(bias, "bias", torch.float32),
-                                 _dev(w_gate, "w_gate", x.dtype), _dev(w_up, "w_up", x.dtype),
-                                 _dev(w_down, "w_down", x.dtype), float(reduce_scale),
-                                 _dev(out, "out", x.dtype), _dev(ws, "ws"), ws.numel(),
-                                 _stream(stream))
-    _check(rc, "foe_cluster_block")
+    args = (_dev(x, "x"), _dev(w_router, "w_router", x.dtype), _dev(bias, "bias", torch.float32),
+            _dev(w_gate, "w_gate", x.dtype), _dev(w_up, "w_up", x.dtype),
+            _dev(w_down, "w_down", x.dtype), float(reduce_scale), _dev(out, "out", x.dtype),
+            _dev(ws, "ws"), ws.numel(), _stream(stream))
+    if gating == "renorm":
+        _check(lib().foe_cluster_block(dt, C, T, d, E, k, F, *args), "foe_cluster_block")
+    else:
+        _check(lib().foe_cluster_block_ex(dt, C, T, d, E, k, F, _gating(gating), *args),
+               "foe_cluster_block_ex")
     return out
 
 

@@ -83,6 +83,32 @@ def test_route_empty_batch_is_a_noop(L):
     assert L.foe_route(BF16, 0, 64, 4, 2, None, None, None, None, None, None) == foe.FOE_OK
 
 
+def test_route_ex_rejects(L):
+    base = [BF16, 2, 16, 64, 4, 2, foe.GATE_GLOBAL, P, P, None, P, P, None]
+    bad = list(base)
+    bad[6] = 2
+    assert L.foe_route_ex(*bad) == INV and "gating must" in foe.last_error()
+    bad = list(base)
+    bad[1] = 0
+    assert L.foe_route_ex(*bad) == INV and "G must" in foe.last_error()
+    big = list(base)
+    big[1], big[4] = 3, 100  # 300 score columns across groups
+    assert L.foe_route_ex(*big) == foe.FOE_ERR_UNSUPPORTED
+    assert L.foe_route_ex(BF16, 2, 0, 64, 4, 2, foe.GATE_RENORM, None, None, None, None, None,
+                          None) == foe.FOE_OK
+
+
+def test_cluster_block_ex_rejects(L):
+    need = L.foe_workspace_bytes(b"cluster_block", BF16, 2, 64, 64, 200, 2, 64)
+    args = [BF16, 2, 64, 64, 200, 2, 64, foe.GATE_GLOBAL, P, P, None, P, P, P,
+            ctypes.c_float(0.5), P, P2, need, None]
+    assert L.foe_cluster_block_ex(*args) == foe.FOE_ERR_UNSUPPORTED
+    assert "global gating" in foe.last_error()
+    bad = list(args)
+    bad[7] = 5
+    assert L.foe_cluster_block_ex(*bad) == INV and "gating must" in foe.last_error()
+
+
 def test_permute_rejects(L):
     need = L.foe_workspace_bytes(b"permute", BF16, 1, 4096, 64, 8, 2, 0)
     assert 0 < need < SIZE_MAX

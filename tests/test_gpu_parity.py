@@ -73,7 +73,7 @@ def stacked(inp):
     return w
 
 
-def check_route(gidx, gw, ref, tol, g64=None):
+def check_route(gidx, gw, ref, tol, g64=None, sums_to_one=True):
     """Compare GPU routing with the oracle's; returns the exempt mask."""
     gidx = np.asarray(gidx).astype(np.int64)
     gw = np.asarray(gw, np.float64)
@@ -88,8 +88,8 @@ def check_route(gidx, gw, ref, tol, g64=None):
     wg = np.take_along_axis(gw[ne], o_g, 1)
     wr = np.take_along_axis(ref["w"][ne], o_r, 1)
     assert rel_err(wg, wr) <= tol, rel_err(wg, wr)
-    # rows of weights sum to one
-    assert np.max(np.abs(gw.sum(1) - 1.0)) <= 1e-5
+    if sums_to_one:  # renormalised gating: rows of weights sum to one
+        assert np.max(np.abs(gw.sum(1) - 1.0)) <= 1e-5
     # exempt tokens still pick a valid top-k of the oracle scores
     g32 = ref["logits"].astype(np.float32).astype(np.float64)
     k = gidx.shape[1]
@@ -140,6 +140,36 @@ def test_route_parity_shapes(T, d, E, k, dt):
     gidx, gw = foe.route(to_dev(xs, dt), to_dev(wr, dt), to_dev(bias, "f32"), k)
     ref = oracle.route(xs, wr, bias, k)
     check_route(host(gidx), host(gw), ref, TOL[dt])
+
+
+@pytest.mark.parametrize("G,T,d,E,k,dt", [
+    (1, 300, 256, 16, 2, "bf16"),   # one group
+    (1, 8200, 136, 20, 3, "bf16"),  # many-token streaming path
+    (1, 40, 32, 16, 16, "f32"),     # k = E: the softmax itself
+    (4, 200, 128, 12, 2, "bf16"),   # four groups in one score matrix
+    (3, 64, 64, 10, 3, "f32"),      # groups straddle the 16-column score tiles
+])
+def test_route_global_gating(G, T, d, E, k, dt):
+    """Global softmax over all G*E scores, not renormalised (foe_route_ex)."""
+    say("route global gating", G, T, d, E, k, dt)
+    rng = np.random.default_rng(T + 31 * G + E)
+    xs = rng.standard_normal((T, d)).astype(np.float32)
+    wr = (rng.standard_normal((G, E, d)) * 0.05).astype(np.float32)
+    bias = (rng.standard_normal((G, E)) * 0.1).astype(np.float32)
+    if dt == "bf16":
+        xs, wr = synth.round_to_bf16(xs), synth.round_to_bf16(wr)
+    w_dev = to_dev(wr if G > 1 else wr[0], dt)
+    b_dev = to_dev(bias if G > 1 else bias[0], "f32")
+    gidx, gw = foe.route(to_dev(xs, dt), w_dev, b_dev, k, gating="global")
+    gidx, gw = host(gidx).reshape(G, T, k), host(gw).reshape(G, T, k)
+    refs = [oracle.route(xs, wr[h], bias[h], k) for h in range(G)]
+    gws = oracle.gate_weights_global([r["logits"] for r in refs], [r["idx"] for r in refs])
+    for h in range(G):
+        check_route(gidx[h], gw[h], dict(refs[h], w=gws[h]), TOL[dt], sums_to_one=False)
+    total = gw.astype(np.float64).sum(axis=(0, 2))
+    assert np.all(total <= 1.0 + 1e-5)
+    if k == E and G == 1:
+        assert np.max(np.abs(total - 1.0)) <= 1e-5
 
 
 @pytest.mark.parametrize("k", [1, 3])
@@ -394,6 +424,26 @@ def test_block_parity_shapes(T, d, E, k, F, C, scale, dt, bias):
     for r in res:
         exempt |= r["margin"] < EXEMPT
     assert rel_err(got[~exempt], ref[~exempt]) <= TOL[dt]
+
+
+@pytest.mark.parametrize("T,d,E,k,F,C", [
+    (128, 256, 16, 2, 128, 1),  # decode form, one cluster
+    (96, 128, 8, 2, 64, 3),     # three clusters, one score matrix
+    (600, 128, 8, 2, 128, 2),   # many pairs per expert: dispatch pass and grouped GEMM
+])
+def test_block_global_gating(T, d, E, k, F, C):
+    say("block global gating", T, d, E, k, F, C)
+    cfg = dict(dtype="bf16", C=C, T=T, d=d, E=E, k=k, F=F, sigma=0.05, seed=T + d + C, bias=None)
+    inp = synth.make_block_inputs(cfg)
+    w = stacked(inp)
+    out = foe.cluster_block(to_dev(inp["x"], "bf16"), w["w_router"], w["bias"], w["w_gate"],
+                            w["w_up"], w["w_down"], k, gating="global")
+    got = host(out)
+    ref, res = oracle.cluster_block(inp["x"], inp["clusters"], k, None, gating="global")
+    exempt = np.zeros(T, dtype=bool)
+    for r in res:
+        exempt |= r["margin"] < EXEMPT
+    assert rel_err(got[~exempt], ref[~exempt]) <= TOL["bf16"]
 
 
 def test_block_is_deterministic():

@@ -112,6 +112,60 @@ def test_gate_weights_invariants():
             assert np.max(np.abs(w - np.sort(p, axis=1)[:, ::-1])) <= 1e-12
 
 
+def test_global_gate_weights_pins():
+    """Global-softmax gating (not renormalised) against the library softmax of
+    the concatenated score vector, and the identities that tie it to the
+    renormalised weights."""
+    rng = np.random.default_rng(17)
+    G, T, E = 3, 200, 8
+    gl = [rng.standard_normal((T, E)) * 1.5 for _ in range(G)]
+    for k in (1, 2, E):
+        idx = [oracle.topk_select(g, k)[0] for g in gl]
+        ws = oracle.gate_weights_global(gl, idx)
+        p = scipy.special.softmax(np.concatenate(gl, axis=1), axis=1)
+        for h in range(G):
+            ref = np.take_along_axis(p, idx[h] + h * E, axis=1)
+            assert np.max(np.abs(ws[h] - ref)) <= 1e-14
+            # renormalising a group's weights gives the renormalised gating
+            r = ws[h] / ws[h].sum(axis=1, keepdims=True)
+            assert np.max(np.abs(r - oracle.gate_weights(gl[h], idx[h]))) <= 1e-12
+        total = sum(w.sum(axis=1) for w in ws)
+        assert np.all(total <= 1.0 + 1e-12)
+        if k == E:
+            assert np.max(np.abs(total - 1.0)) <= 1e-12
+        # unchanged when a constant is added to every score of every group
+        for a, b in zip(ws, oracle.gate_weights_global([g - 40.0 for g in gl], idx)):
+            assert np.max(np.abs(a - b)) <= 1e-12
+    # one group and k = E: the global softmax is the renormalised softmax
+    idx = oracle.topk_select(gl[0], E)[0]
+    assert np.max(np.abs(oracle.gate_weights_global([gl[0]], [idx])[0]
+                         - oracle.gate_weights(gl[0], idx))) <= 1e-12
+
+
+def test_global_gating_block_special_cases():
+    """The block with global gating: one cluster with k = E equals the
+    renormalised block; with C clusters each delta is scaled by the cluster's
+    share of the probability mass relative to the renormalised one."""
+    rng = np.random.default_rng(23)
+    x = rng.standard_normal((12, 8)).astype(np.float32)
+    cl = _small_cluster(4, 8, 12, seed=23)
+    a, _ = oracle.cluster_block(x, [cl], 4, reduce_scale=1.0, gating="global")
+    b, _ = oracle.cluster_block(x, [cl], 4, reduce_scale=1.0)
+    assert np.max(np.abs(a - b)) <= 1e-12
+    # k = 1 in every cluster: delta_h = p_h(selected) * FFN(x) for the top expert
+    cls = [_small_cluster(4, 8, 12, seed=30 + h) for h in range(2)]
+    out, res = oracle.cluster_block(x, cls, 1, reduce_scale=1.0, gating="global")
+    g = np.concatenate([oracle.router_logits(x, c["w_router"]) for c in cls], axis=1)
+    p = scipy.special.softmax(g, axis=1)
+    ref = 2 * x.astype(np.float64)
+    for h, c in enumerate(cls):
+        e = res[h]["idx"][:, 0]
+        for i in range(x.shape[0]):
+            f = oracle.swiglu_ffn(x[i:i + 1], c["w_gate"][e[i]], c["w_up"][e[i]], c["w_down"][e[i]])
+            ref[i] += p[i, h * 4 + e[i]] * f[0]
+    assert np.max(np.abs(out - ref)) <= 1e-12
+
+
 def test_histogram_bruteforce():
     idx = synth.make_topk_idx(37, 6, 3, seed=1, skew=1.0, dead_experts=(4,))
     counts, offsets = oracle.expert_histogram(idx, 6)
