@@ -1,7 +1,8 @@
 // Weighted un-permute-combine (Table 3 "MoE update") and the local reduction
 // of cluster partials (Table 3 "Cross-group avg."; Section 3.2).  Both are
-// HBM-bound row streams: one wave per token row, 128-bit loads and stores,
-// fp32 accumulation in a fixed order.
+// HBM-bound row streams with 128-bit loads and stores and fp32 accumulation
+// in a fixed order: the step-wise combine takes one wave per token row, the
+// block's combine one wave per (token, chunk of the row).
 #include "foe_common.hpp"
 
 #ifndef FOE_COMBINE_U

@@ -1,6 +1,6 @@
 // C ABI of the per-cluster MoE block library (declarations and contracts in
 // include/foe.h).  Host code only: argument checks, workspace carving, the
-// per-cluster launch sequence and the kernel-timing registry.
+// launch sequence of the block and the kernel-timing registry.
 #include <limits.h>
 
 #include <mutex>

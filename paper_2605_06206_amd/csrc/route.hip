@@ -1,14 +1,20 @@
-// Router scores + per-group top-k + softmax weights (Section 3.1, routing
-// equation), fused in one kernel: the [T,E] scores never leave the chip.
+// Router scores + per-group top-k + routing weights (Section 3.1, routing
+// equation), fused in one kernel: the [T, G*E] scores never leave the chip.
 //
-// One workgroup = TG groups of 16 tokens, 4 or 8 waves.  The score tile
-// S[16 tokens][E] of each group is a skinny GEMM x[16,d] * W_r[E,d]^T on MFMA
-// (bf16: 16x16x32, fp32: 16x16x4) with K split across the waves (each issuing
-// the loads of several K steps at once); the partial tiles are summed in LDS
-// in a fixed order.  In the 16x16
-// MFMA result layout each row of 16 lanes holds all 16 experts of one token
-// (per accumulator register), so the top-k is k rounds of a (score desc, id
-// asc) arg-max across a 16-lane row with DPP rotations.
+// route_kernel: one workgroup = TG groups of 16 tokens, 4 or 8 waves.  The
+// score tile S[16 tokens][G*E] of each token group is x[16,d] * W_r^T on
+// MFMA (bf16: 16x16x32, fp32: 16x16x4) with K split across the waves (each
+// issuing the loads of several K steps at once); the partial tiles are summed
+// in LDS in a fixed order.  G router matrices of co-resident clusters are one
+// score matrix, so x is read once for all of them.  In the 16x16 MFMA result
+// layout each row of 16 lanes holds 16 score columns of one token (per
+// accumulator register), so a group's top-k is k rounds of a (score desc, id
+// asc) arg-max over the group's columns across a 16-lane row with DPP
+// rotations.  route_stream_kernel (many tokens, one group, E <= 32) streams x
+// and W_r through LDS with a wave per 16 tokens over all of K.
+//
+// Weights: the softmax over the k selected scores of the group, or (global
+// gating) the softmax over all G*E scores of the token, not renormalised.
 #include "lds_dma.hpp"
 
 namespace foe {
