@@ -115,6 +115,46 @@ def make_block_inputs(cfg, T=None, weight_set=0):
 
 
 # ---------------------------------------------------------------------------
+# Per-group attention that feeds the block (H groups, one KV head each)
+# ---------------------------------------------------------------------------
+
+# shapes of the paper's 7B model per group: 16 query / 8 KV heads over H = 8
+# groups (nq = 2 query heads share each group's KV head), head dim 128, RoPE
+# base 500000 with scaling factor 16; S tokens of one prefill chunk
+ATTN_CONFIGS = {
+    "attn_tiny_bf16": dict(H=2, S=200, d=256, nq=2, hd=128, theta=500000.0, scale=16.0,
+                           sigma=0.05, seed=6),
+    "attn_share_bf16": dict(H=8, S=4096, d=2048, nq=2, hd=128, theta=500000.0, scale=16.0,
+                            sigma=0.02, seed=5),
+}
+
+
+def make_attention_inputs(cfg, weight_set=0):
+    """Inputs of one per-group attention pass for a config (name or dict).
+
+    ``x ~ N(0,1) [H,S,d]`` (one representation per group) from
+    ``default_rng(seed + 7919*weight_set)``; group ``h``'s ``w_qkv``
+    [(nq+2)*hd, d] and ``w_o`` [d, nq*hd] ~ N(0, sigma) from
+    ``default_rng([seed + 7919*weight_set, 100 + h])``.  Every tensor is
+    rounded to bf16.  Returns a dict with ``cfg``, ``x`` and ``groups``.
+    """
+    if isinstance(cfg, str):
+        cfg = dict(ATTN_CONFIGS[cfg], name=cfg)
+    else:
+        cfg = dict(cfg)
+    wseed = cfg["seed"] + 7919 * weight_set
+    rng = np.random.default_rng(wseed)
+    H, S, d, nq, hd = cfg["H"], cfg["S"], cfg["d"], cfg["nq"], cfg["hd"]
+    x = round_to_bf16(rng.standard_normal((H, S, d), dtype=np.float32))
+    groups = []
+    for h in range(H):
+        g = np.random.default_rng([wseed, 100 + h])
+        groups.append({"w_qkv": round_to_bf16(_normal(g, ((nq + 2) * hd, d), cfg["sigma"])),
+                       "w_o": round_to_bf16(_normal(g, (d, nq * hd), cfg["sigma"]))})
+    return {"cfg": cfg, "x": x, "groups": groups}
+
+
+# ---------------------------------------------------------------------------
 # Inputs for exercising one step on its own (decoupled from upstream steps)
 # ---------------------------------------------------------------------------
 
