@@ -230,6 +230,32 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
                          void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * foe_group_attention - the per-group attention that feeds the block (Table 3,
+ * FoE column, rows "Attn. residual" and "Cross-group avg."):
+ *   r[h,i]    = x[h,i] + Attn_h(x[h,:])[i]     (every group its own representation)
+ *   r_full[i] = (1/H) sum_h r[h,i]             (fp32, h = 0..H-1 in order)
+ * Attn_h: causal self-attention over the S tokens (positions 0..S-1) with one
+ * key/value head and nq query heads sharing it (grouped-query attention),
+ * scores q.k/sqrt(hd), rotary embedding on q and k pairing dimension i with
+ * i+hd/2 at angle (s/scale)*theta^(-2i/hd), bias-free projections.
+ *
+ *   x        [H,S,d]          bf16
+ *   w_qkv    [H,(nq+2)*hd,d]  bf16  rows: nq query heads, the key head, the value head
+ *   w_o      [H,d,nq*hd]      bf16
+ *   theta    rotary base (> 0);  scale: rotary scaling factor (> 0), positions / scale
+ *   r_full   [S,d]            bf16 out
+ *   ws, ws_bytes              workspace of foe_group_attention_workspace_bytes()
+ * bf16 only and hd = 128 (else FOE_ERR_UNSUPPORTED); H*S*d, H*S*(nq+2)*hd below
+ * 2^30 elements.
+ */
+int foe_group_attention(foe_dtype dt, int H, int S, int d, int nq, int hd, float theta,
+                        float scale, const void* x, const void* w_qkv, const void* w_o,
+                        void* r_full, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes of foe_group_attention (SIZE_MAX for invalid sizes). */
+size_t foe_group_attention_workspace_bytes(int H, int S, int d, int nq, int hd);
+
+/*
  * foe_workspace_bytes - workspace size in bytes for `op` (host string:
  * "route", "permute", "expert_ffn", "combine", "reduce", "cluster_block").
  * Arguments an op does not use are ignored (pass 0); for "expert_ffn" T is the

@@ -34,7 +34,8 @@ from __future__ import annotations
 
 import numpy as np
 
-__all__ = ["rope_angles", "apply_rope", "group_attention", "attention_block"]
+__all__ = ["rope_angles", "apply_rope", "group_attention", "group_attention_rows",
+           "attention_block"]
 
 
 def _f64(a):
@@ -87,6 +88,29 @@ def group_attention(xh, w_qkv, w_o, nq, hd, theta, scale=1.0):
         o[:, j] = p @ v
     o = o.reshape(S, nq * hd)
     return o @ _f64(w_o).T, {"q": q, "k": k, "v": v, "o": o}
+
+
+def group_attention_rows(xh, w_qkv, w_o, nq, hd, theta, scale, rows):
+    """``Attn_h(x[h, :])`` at the positions ``rows`` only (the same definition
+    as ``group_attention``; keys and values are formed for every position up
+    to the last requested one).  Returns [len(rows), d]."""
+    xh = _f64(xh)
+    rows = np.asarray(rows)
+    last = int(rows.max()) + 1
+    w_qkv = _f64(w_qkv)
+    kv = xh[:last] @ w_qkv[nq * hd:].T
+    cos, sin = rope_angles(last, hd, theta, scale)
+    k = apply_rope(kv[:, :hd], cos, sin)
+    v = kv[:, hd:]
+    q_all = xh[rows] @ w_qkv[: nq * hd].T
+    out = np.zeros((len(rows), nq * hd))
+    for n, s in enumerate(rows):
+        for j in range(nq):
+            q = apply_rope(q_all[n:n + 1, j * hd:(j + 1) * hd], cos[s:s + 1], sin[s:s + 1])[0]
+            sc = (k[: s + 1] @ q) / np.sqrt(hd)
+            p = np.exp(sc - sc.max())
+            out[n, j * hd:(j + 1) * hd] = (p / p.sum()) @ v[: s + 1]
+    return out @ _f64(w_o).T
 
 
 def attention_block(x, groups, nq, hd, theta, scale=1.0):

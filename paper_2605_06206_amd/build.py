@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG_DIR, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG_DIR, "libfoe.so")
 
-SOURCES = ["foe_api.hip", "route.hip", "permute.hip", "ffn.hip", "combine.hip"]
+SOURCES = ["foe_api.hip", "route.hip", "permute.hip", "ffn.hip", "combine.hip", "attention.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -1004,6 +1004,16 @@ hipError_t launch_expert_ffn_sel(int C, int E, int d, int F, int T, int k, const
   return hipGetLastError();
 }
 
+hipError_t launch_grouped_gemm(const void* A, const int32_t* offsets, int E, int rows,
+                               const void* W, int N, int K, void* out, hipStream_t s,
+                               const char* name) {
+  if (rows == 0) return hipSuccess;
+  DmaLaunch<FOE_DMA_DN>::run<false>(static_cast<const bf16*>(A), (const int32_t*)nullptr, 1, rows,
+                                    offsets, E, rows, static_cast<const bf16*>(W),
+                                    (const bf16*)nullptr, N, K, static_cast<bf16*>(out), s, name);
+  return hipGetLastError();
+}
+
 hipError_t launch_expert_ffn(foe_dtype dt, int E, int d, int F, int rows, const void* x_perm,
                              const int32_t* offsets, const void* w_gate, const void* w_up,
                              const void* w_down, void* y_perm, void* scratch, hipStream_t s) {

@@ -432,6 +432,53 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
   return FOE_OK;
 }
 
+size_t foe_group_attention_workspace_bytes(int H, int S, int d, int nq, int hd) {
+  Check c;
+  c.need(H >= 1 && H <= 64, "H must be in [1, 64]");
+  c.need(S >= 0, "S must be >= 0");
+  check_dim8(c, d, "d must be a positive multiple of 8");
+  c.need(nq >= 1 && nq <= 64, "nq must be in [1, 64]");
+  c.need(hd == 128, "hd must be 128");
+  if (!c.err.empty()) return (g_err = c.err, SIZE_MAX);
+  return group_attention_scratch_bytes(H, S, d, nq, hd);
+}
+
+int foe_group_attention(foe_dtype dt, int H, int S, int d, int nq, int hd, float theta,
+                        float scale, const void* x, const void* w_qkv, const void* w_o,
+                        void* r_full, void* ws, size_t ws_bytes, void* stream) {
+  Check c;
+  check_dtype(c, dt);
+  c.need(H >= 1 && H <= 64, "H must be in [1, 64]");
+  c.need(S >= 0, "S must be >= 0");
+  check_dim8(c, d, "d must be a positive multiple of 8");
+  c.need(nq >= 1 && nq <= 64, "nq must be in [1, 64]");
+  c.need(theta > 0.f && scale > 0.f, "theta and scale must be > 0");
+  const bool any = S > 0;
+  c.tensor(x, any, "x");
+  c.tensor(w_qkv, any, "w_qkv");
+  c.tensor(w_o, any, "w_o");
+  c.tensor(r_full, any, "r_full");
+  if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_group_attention: " + c.err);
+  if (dt != FOE_BF16 || hd != 128)
+    return fail(FOE_ERR_UNSUPPORTED, "foe_group_attention: bf16 with hd = 128 only");
+  const long long rows = (long long)H * S;
+  if (!(operand_fits(rows, d, 2) && operand_fits(rows, (long long)(nq + 2) * hd, 2)))
+    return fail(FOE_ERR_UNSUPPORTED,
+                "foe_group_attention: H*S*d and H*S*(nq+2)*hd must stay below 2^30");
+  if (!any) return FOE_OK;
+  const size_t need = group_attention_scratch_bytes(H, S, d, nq, hd);
+  if (ws == nullptr || !aligned16(ws))
+    return fail(FOE_ERR_INVALID, "foe_group_attention: ws is NULL or not 16-byte aligned");
+  if (ws_bytes < need)
+    return fail(FOE_ERR_WORKSPACE, "foe_group_attention: workspace needs " +
+                                       std::to_string(need) + " bytes, got " +
+                                       std::to_string(ws_bytes));
+  hipError_t e = launch_group_attention(H, S, d, nq, hd, theta, scale, x, w_qkv, w_o, r_full, ws,
+                                        reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "foe_group_attention");
+  return FOE_OK;
+}
+
 int foe_profile_enable(int on) {
   std::lock_guard<std::mutex> lock(g_prof_mu);
   g_prof_on = on != 0;

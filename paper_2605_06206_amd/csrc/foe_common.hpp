@@ -116,6 +116,18 @@ hipError_t launch_expert_ffn(foe_dtype dt, int E, int d, int F, int rows, const 
                              const int32_t* offsets, const void* w_gate, const void* w_up,
                              const void* w_down, void* y_perm, void* scratch, hipStream_t s);
 
+// bf16 grouped GEMM out[r] = A[r] W[e]^T for the rows r of segment e
+// (offsets [E+1]); W [E, N, K], A [rows, K], out [rows, N] (the down-projection
+// kernel of the expert FFN)
+hipError_t launch_grouped_gemm(const void* A, const int32_t* offsets, int E, int rows,
+                               const void* W, int N, int K, void* out, hipStream_t s,
+                               const char* name);
+// per-group attention of Table 3 (attention.hip): r_full [S, d] from x [H, S, d]
+size_t group_attention_scratch_bytes(int H, int S, int d, int nq, int hd);
+hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float theta, float scale,
+                                  const void* x, const void* w_qkv, const void* w_o, void* r_full,
+                                  void* scratch, hipStream_t s);
+
 // expert FFN whose operand row r is row gather[r]/kdiv of A (a_rows rows);
 // gather == nullptr: row r of A
 hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, const void* A,

@@ -47,6 +47,9 @@ _SIGNATURES = {
                                       _p]),
     "foe_workspace_bytes": (_c_size, [ctypes.c_char_p, _c_int, _c_int, _c_int, _c_int, _c_int,
                                       _c_int, _c_int]),
+    "foe_group_attention": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_float,
+                                     _c_float, _p, _p, _p, _p, _p, _c_size, _p]),
+    "foe_group_attention_workspace_bytes": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
     "foe_last_error": (ctypes.c_char_p, []),
     "foe_profile_enable": (_c_int, [_c_int]),
     "foe_profile_reset": (_c_int, []),
@@ -254,6 +257,28 @@ def cluster_block(x, w_router, bias, w_gate, w_up, w_down, k, reduce_scale=None,
     else:
         _check(lib().foe_cluster_block_ex(dt, C, T, d, E, k, F, _gating(gating), *args),
                "foe_cluster_block_ex")
+    return out
+
+
+def group_attention(x, w_qkv, w_o, nq, theta, scale=1.0, out=None, ws=None, stream=None):
+    """foe_group_attention: x [H,S,d], w_qkv [H,(nq+2)*hd,d], w_o [H,d,nq*hd]
+    (bf16, hd = 128) -> r_full [S,d]."""
+    H, S, d = x.shape
+    hd = w_qkv.shape[1] // (nq + 2)
+    if tuple(w_qkv.shape) != (H, (nq + 2) * hd, d) or tuple(w_o.shape) != (H, d, nq * hd):
+        raise FoeError(FOE_ERR_INVALID, f"group_attention: w_qkv {tuple(w_qkv.shape)} / w_o "
+                       f"{tuple(w_o.shape)} do not match x {tuple(x.shape)} with nq={nq}")
+    if out is None:
+        out = torch.empty((S, d), dtype=x.dtype, device=x.device)
+    n = lib().foe_group_attention_workspace_bytes(H, S, d, nq, hd)
+    if n == ctypes.c_size_t(-1).value:
+        raise FoeError(FOE_ERR_INVALID, f"foe_group_attention_workspace_bytes: {last_error()}")
+    ws = _workspace(ws, n, x.device)
+    rc = lib().foe_group_attention(_dt(x), H, S, d, nq, hd, float(theta), float(scale),
+                                   _dev(x, "x"), _dev(w_qkv, "w_qkv", x.dtype),
+                                   _dev(w_o, "w_o", x.dtype), _dev(out, "r_full", x.dtype),
+                                   _dev(ws, "ws"), ws.numel(), _stream(stream))
+    _check(rc, "foe_group_attention")
     return out
 
 

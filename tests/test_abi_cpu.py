@@ -109,6 +109,34 @@ def test_cluster_block_ex_rejects(L):
     assert L.foe_cluster_block_ex(*bad) == INV and "gating must" in foe.last_error()
 
 
+def test_group_attention_rejects(L):
+    n = L.foe_group_attention_workspace_bytes(8, 4096, 2048, 2, 128)
+    assert 0 < n < SIZE_MAX
+    assert L.foe_group_attention_workspace_bytes(8, 4096, 2048, 2, 64) == SIZE_MAX
+    assert "hd must be 128" in foe.last_error()
+    f = ctypes.c_float
+    ok = [BF16, 2, 64, 64, 2, 128, f(500000.0), f(16.0), P, P, P, P]
+    bad = list(ok)
+    bad[5] = 96
+    assert L.foe_group_attention(*bad, P2, n, None) == foe.FOE_ERR_UNSUPPORTED
+    bad = list(ok)
+    bad[0] = F32
+    assert L.foe_group_attention(*bad, P2, n, None) == foe.FOE_ERR_UNSUPPORTED
+    bad = list(ok)
+    bad[1] = 0
+    assert L.foe_group_attention(*bad, P2, n, None) == INV and "H must" in foe.last_error()
+    bad = list(ok)
+    bad[6] = f(0.0)
+    assert L.foe_group_attention(*bad, P2, n, None) == INV and "theta" in foe.last_error()
+    bad = list(ok)
+    bad[8] = None
+    assert L.foe_group_attention(*bad, P2, n, None) == INV and "x is NULL" in foe.last_error()
+    need = L.foe_group_attention_workspace_bytes(2, 64, 64, 2, 128)
+    assert L.foe_group_attention(*ok, P2, need - 256, None) == WS
+    assert L.foe_group_attention(BF16, 2, 0, 64, 2, 128, f(500000.0), f(16.0), None, None, None,
+                                 None, None, 0, None) == foe.FOE_OK
+
+
 def test_permute_rejects(L):
     need = L.foe_workspace_bytes(b"permute", BF16, 1, 4096, 64, 8, 2, 0)
     assert 0 < need < SIZE_MAX

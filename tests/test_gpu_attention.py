@@ -1,0 +1,92 @@
+"""GPU parity of the per-group attention (foe_group_attention) against the
+oracle, on the C ABI through the binding."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention_oracle as ao
+from paper_2605_06206_amd import foe, synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+TOL = 2e-2  # bf16 storage of q/k/v, p, o and the attention output
+
+
+def say(*a):
+    print("[attn]", *a, flush=True)
+
+
+def to_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV).to(torch.bfloat16)
+
+
+def rel_err(got, ref):
+    return float(np.max(np.abs(got - ref)) / max(np.max(np.abs(ref)), 1e-30))
+
+
+def _run(inp):
+    c = inp["cfg"]
+    x = to_dev(inp["x"])
+    w_qkv = to_dev(np.stack([g["w_qkv"] for g in inp["groups"]]))
+    w_o = to_dev(np.stack([g["w_o"] for g in inp["groups"]]))
+    out = foe.group_attention(x, w_qkv, w_o, c["nq"], c["theta"], c["scale"])
+    torch.cuda.synchronize()
+    return out.float().cpu().numpy()
+
+
+def _check(inp, got):
+    c = inp["cfg"]
+    ref, _ = ao.attention_block(inp["x"], inp["groups"], c["nq"], c["hd"], c["theta"], c["scale"])
+    # the attention part alone as well (the residual dominates r_full)
+    xm = inp["x"].astype(np.float64).mean(axis=0)
+    e_full, e_attn = rel_err(got, ref), rel_err(got - xm, ref - xm)
+    say(f"rel err r_full {e_full:.2e}, attention part {e_attn:.2e}")
+    assert e_full <= TOL and e_attn <= TOL
+
+
+@pytest.mark.parametrize("H,S,d,nq,theta,scale", [
+    (2, 200, 256, 2, 500000.0, 16.0),   # ragged last query / key block
+    (1, 1, 64, 2, 500000.0, 16.0),      # one token
+    (3, 65, 64, 1, 10000.0, 1.0),       # odd query-head count, one key past a block
+    (2, 130, 136, 4, 500000.0, 16.0),   # four query heads per key head, d off the tiles
+    (1, 512, 128, 2, 500000.0, 1.0),    # eight key blocks, long-range rotary angles
+])
+def test_group_attention_parity(H, S, d, nq, theta, scale):
+    say("parity", H, S, d, nq, theta, scale)
+    cfg = dict(H=H, S=S, d=d, nq=nq, hd=128, theta=theta, scale=scale, sigma=0.05,
+               seed=H * 1000 + S)
+    inp = synth.make_attention_inputs(cfg)
+    _check(inp, _run(inp))
+
+
+def test_group_attention_full_size_sampled():
+    """The 8-group, 4096-token configuration: sampled query rows (first, block
+    edges, last) against the per-row oracle."""
+    inp = synth.make_attention_inputs("attn_share_bf16")
+    c = inp["cfg"]
+    say("full size", c)
+    got = _run(inp)
+    rows = [0, 1, 63, 64, 1000, 2047, 2048, 3071, 4095]
+    x = inp["x"].astype(np.float64)
+    ref = np.zeros((len(rows), c["d"]))
+    for h, g in enumerate(inp["groups"]):
+        ref += x[h, rows] + ao.group_attention_rows(x[h], g["w_qkv"], g["w_o"], c["nq"], c["hd"],
+                                                    c["theta"], c["scale"], rows)
+    ref /= c["H"]
+    xm = x[:, rows].mean(axis=0)
+    e_full, e_attn = rel_err(got[rows], ref), rel_err(got[rows] - xm, ref - xm)
+    say(f"rel err r_full {e_full:.2e}, attention part {e_attn:.2e}")
+    assert e_full <= TOL and e_attn <= TOL
+
+
+def test_group_attention_deterministic_and_empty():
+    inp = synth.make_attention_inputs("attn_tiny_bf16")
+    say("determinism")
+    a = _run(inp)
+    b = _run(inp)
+    assert np.array_equal(a, b)
+    e = foe.group_attention(torch.empty((2, 0, 64), dtype=torch.bfloat16, device=DEV),
+                            torch.empty((2, 512, 64), dtype=torch.bfloat16, device=DEV),
+                            torch.empty((2, 64, 256), dtype=torch.bfloat16, device=DEV), 2,
+                            500000.0)
+    assert e.shape == (0, 64)
