@@ -11,6 +11,11 @@ Default workload: the decode-shaped cluster block (T=128, d=2048, E=16, k=2,
 F=1024, bf16).  Several independent weight/input sets are rotated so the
 working set exceeds the 256 MB Infinity Cache.
 
+`--config attn_share_bf16` (or another attention configuration) times the
+per-group attention that feeds the block instead: one step = one
+foe_group_attention call (H=8 groups, S=4096 tokens, d=2048, two query heads of
+128 per group sharing its key/value head, causal).
+
 `traffic` in the roofline object is the measured HBM traffic per launch of the
 dominant kernel (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by what the same
 counters read for a plain copy of known size: `--copy-calibration`), read from
@@ -66,7 +71,9 @@ KERNEL_SOURCES = {"route": "route.hip", "permute_index": "permute.hip",
                   "permute_hist": "permute.hip", "permute_rank": "permute.hip",
                   "permute_scan": "permute.hip", "permute_scatter": "permute.hip",
                   "ffn_gateup": "ffn.hip", "ffn_down": "ffn.hip", "ffn_gateup_f32": "ffn.hip",
-                  "ffn_down_f32": "ffn.hip", "combine": "combine.hip", "reduce": "combine.hip"}
+                  "ffn_down_f32": "ffn.hip", "combine": "combine.hip", "reduce": "combine.hip",
+                  "attn_qkv": "ffn.hip", "attn_out": "ffn.hip", "attn_prep": "attention.hip",
+                  "attn_core": "attention.hip", "attn_resid_avg": "attention.hip"}
 
 
 def source_sha(kernel):
@@ -110,6 +117,8 @@ def kernel_work(name, cfg, e_touched):
     experts' pairs itself), the two grouped FFN kernels (all C*E experts) and
     the combine + reduction.  `e_touched` = experts (over all clusters) that
     got rows."""
+    if "nq" in cfg:
+        return attention_work(name, cfg)
     T, d, E, k, F, C = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["F"], cfg["C"]
     s = 2 if cfg["dtype"] == "bf16" else 4
     R = T * k          # pairs per cluster
@@ -127,6 +136,33 @@ def kernel_work(name, cfg, e_touched):
     return 0.0, 0.0
 
 
+def attention_work(name, cfg):
+    """Algorithmic (flops, bytes) of ONE launch of kernel `name` in a
+    foe_group_attention call (H groups, S tokens, nq query heads of dim hd per
+    group, bf16).  The causal attention counts the scores and the value
+    products of the S(S+1)/2 visible (query, key) pairs only."""
+    H, S, d, nq, hd = cfg["H"], cfg["S"], cfg["d"], cfg["nq"], cfg["hd"]
+    rows = H * S
+    n_qkv = (nq + 2) * hd
+    if name == "attn_qkv":
+        return 2.0 * rows * d * n_qkv, 2.0 * (rows * d + H * n_qkv * d + rows * n_qkv)
+    if name == "attn_prep":
+        # q and k read and written back rotated; v read, written transposed
+        # (keys padded to a multiple of 64)
+        s_pad = -(-S // 64) * 64
+        return 0.0, 2.0 * (2 * rows * (nq + 1) * hd + rows * hd + H * hd * s_pad)
+    if name == "attn_core":
+        # bytes: q, k and v once and o once (the query blocks' re-reads of k
+        # and v are not algorithmic)
+        return (4.0 * hd * nq * H * S * (S + 1) / 2,
+                2.0 * (rows * n_qkv + rows * nq * hd))
+    if name == "attn_out":
+        return 2.0 * rows * nq * hd * d, 2.0 * (rows * nq * hd + H * d * nq * hd + rows * d)
+    if name == "attn_resid_avg":
+        return 0.0, 2.0 * (2 * rows * d + S * d)
+    return 0.0, 0.0
+
+
 def roofline(name, cfg, e_touched, avg_s):
     flops, nbytes = kernel_work(name, cfg, e_touched)
     if cfg["dtype"] == "f32" and name.startswith("ffn"):
@@ -141,13 +177,9 @@ def roofline(name, cfg, e_touched, avg_s):
             "bytes_per_launch": nbytes}
 
 
-def cpu_baseline(cfg_name, budget_s):
-    """The oracle as it stands, timed on this host's cores on a bounded sample."""
-    import numpy as np
-
-    import oracle
-    from paper_2605_06206_amd import synth
-
+def cpu_threads():
+    """(threads of the BLAS pools numpy uses, their names)."""
+    import numpy  # noqa: F401  (loads the BLAS whose pools are listed)
     try:
         from threadpoolctl import threadpool_info
         pools = threadpool_info()
@@ -155,6 +187,17 @@ def cpu_baseline(cfg_name, budget_s):
         blas = ",".join(sorted({p.get("internal_api", "?") for p in pools}))
     except Exception:  # pragma: no cover - informational only
         threads, blas = os.cpu_count(), "unknown"
+    return threads, blas
+
+
+def cpu_baseline(cfg_name, budget_s):
+    """The oracle as it stands, timed on this host's cores on a bounded sample."""
+    import numpy as np
+
+    import oracle
+    from paper_2605_06206_amd import synth
+
+    threads, blas = cpu_threads()
     cfg = dict(synth.CONFIGS[cfg_name])
     # a token prefix small enough for ~1 s per oracle call
     per_tok = cfg["C"] * (cfg["k"] * 6.0 * cfg["d"] * cfg["F"] + 2.0 * cfg["d"] * cfg["E"])
@@ -175,6 +218,159 @@ def cpu_baseline(cfg_name, budget_s):
                       f"affinity {len(os.sched_getaffinity(0))} cpus"}
 
 
+def timed_on(stream, n_steps, run):
+    """Milliseconds of n_steps calls of run(i), HIP events on `stream`."""
+    import torch
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for i in range(n_steps):
+        run(i)
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b)
+
+
+def kernel_profile(foe, n_steps, run):
+    """Pass B: every library kernel bracketed by HIP events -> (total ms,
+    {name: launches, avg_us, total_ms})."""
+    foe.profile_reset()
+    foe.profile_enable(True)
+    t_b = run(n_steps)
+    foe.profile_enable(False)
+    kernels = {}
+    for name in foe.profile_names():
+        n, tot = foe.profile_kernel(name)
+        kernels[name] = {"launches": n, "avg_us": round(tot / n * 1e3, 3), "total_ms": tot}
+    foe.profile_reset()
+    return t_b, kernels
+
+
+def cpu_baseline_attention(cfg, inp, budget_s):
+    """The attention oracle as it stands, on a bounded sample of query rows of
+    every group (the keys and values up to the last sampled row are formed
+    each time, as the definition needs)."""
+    import numpy as np
+
+    from oracle import attention_oracle as ao
+    S = cfg["S"]
+    rows = np.arange(0, S, max(1, S // 16))
+    x = inp["x"].astype(np.float64)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        for h, g in enumerate(inp["groups"]):
+            ao.group_attention_rows(x[h], g["w_qkv"], g["w_o"], cfg["nq"], cfg["hd"],
+                                    cfg["theta"], cfg["scale"], rows)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 100:
+            break
+    threads, blas = cpu_threads()
+    return {"value": round(reps * len(rows) / el, 2), "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{reps} oracle runs (fp64 numpy) of {len(rows)} query rows spread over "
+                      f"the {S} positions, all {cfg['H']} groups, {el:.1f} s, BLAS {blas}"}
+
+
+def main_attention(args):
+    """One step = one foe_group_attention call (q/k/v projection, rotary
+    embedding, causal attention, output projection, residual average over the
+    groups) on one sequence resident in HBM."""
+    import numpy as np
+    import torch
+
+    from paper_2605_06206_amd import foe, synth
+
+    torch.cuda.set_device(0)
+    dev = "cuda:0"
+    inp = synth.make_attention_inputs(args.config)
+    cfg = dict(inp["cfg"], name=args.config, dtype="bf16")
+    H, S, d, nq, hd = cfg["H"], cfg["S"], cfg["d"], cfg["nq"], cfg["hd"]
+
+    def up(a):
+        return torch.from_numpy(synth.bf16_bits(a)).to(dev).view(torch.bfloat16)
+
+    x = up(inp["x"])
+    w_qkv = up(np.stack([g["w_qkv"] for g in inp["groups"]]))
+    w_o = up(np.stack([g["w_o"] for g in inp["groups"]]))
+    out = torch.empty((S, d), dtype=torch.bfloat16, device=dev)
+    L = foe.lib()
+    ws_n = L.foe_group_attention_workspace_bytes(H, S, d, nq, hd)
+    ws = torch.empty(ws_n, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    sraw = stream.cuda_stream
+    call = (foe.BF16, H, S, d, nq, hd, float(cfg["theta"]), float(cfg["scale"]), x.data_ptr(),
+            w_qkv.data_ptr(), w_o.data_ptr(), out.data_ptr(), ws.data_ptr(), ws_n)
+
+    def step(i, s):
+        rc = L.foe_group_attention(*call, s)
+        if rc != 0:
+            raise RuntimeError(foe.last_error())
+
+    for i in range(args.warmup):
+        step(i, sraw)
+    eager_ms = timed_on(stream, args.steps, lambda i: step(i, sraw)) / args.steps
+    graph_ms = None
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            step(0, side.cuda_stream)
+        step(0, sraw)
+        torch.cuda.synchronize()
+        ref = out.clone()
+        out.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        if not torch.equal(out, ref):
+            raise RuntimeError("graph replay differs from the eager call")
+        for _ in range(args.warmup):
+            g.replay()
+        graph_ms = timed_on(stream, args.steps, lambda i: g.replay()) / args.steps
+    use_graph = graph_ms is not None and graph_ms < eager_ms
+    ms = graph_ms if use_graph else eager_ms
+
+    t_b, kernels = kernel_profile(
+        foe, args.steps, lambda n: timed_on(stream, n, lambda i: step(i, sraw)))
+    dom = max(kernels, key=lambda n: kernels[n]["total_ms"])
+    roof = roofline(dom, cfg, 0, kernels[dom]["avg_us"] * 1e-6)
+    roof["traffic"] = measured_traffic(args.config, dom)
+    per_kernel_roof = {n: roofline(n, cfg, 0, v["avg_us"] * 1e-6)
+                       for n, v in kernels.items() if sum(attention_work(n, cfg)) > 0}
+    flops = sum(attention_work(n, cfg)[0] for n in ("attn_qkv", "attn_core", "attn_out"))
+    line = {
+        "metric": "tokens/s of the per-group attention feeding the FoE block, 1 GPU",
+        "value": round(S / (ms * 1e-3), 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) activations, N(0,sigma) weights)",
+        "config": {"workload": f"{args.config}: H={H} S={S} d={d} nq={nq} hd={hd} bf16, causal",
+                   "H": H, "S": S, "d": d, "nq": nq, "hd": hd,
+                   "launch": "hip_graph_replay" if use_graph else "eager"},
+        "attention_tflops": round(flops / (ms * 1e-3) / 1e12, 3),
+        "eager_ms_per_step": round(eager_ms, 6),
+        "graph_ms_per_step": None if graph_ms is None else round(graph_ms, 6),
+        "profiled_ms_per_step": round(t_b / args.steps, 6),
+        "roofline": roof,
+        "kernels": {n: {"avg_us": v["avg_us"], "launches_per_step": v["launches"] / args.steps,
+                        **({"frac": per_kernel_roof[n]["frac"], "bound": per_kernel_roof[n]["bound"]}
+                           if n in per_kernel_roof else {})}
+                    for n, v in kernels.items()},
+        "cpu_baseline": None,
+    }
+    if args.cpu_seconds > 0:
+        line["cpu_baseline"] = cpu_baseline_attention(cfg, inp, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -193,6 +389,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.config in synth.ATTN_CONFIGS:
+        main_attention(args)
+        return
     torch.cuda.set_device(0)
     dev = "cuda:0"
     cfg = dict(synth.CONFIGS[args.config], name=args.config)
@@ -249,15 +448,7 @@ def main():
         e_touched += int((p["counts"] > 0).sum().item())
 
     def timed(n_steps, run):
-        torch.cuda.synchronize()
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for i in range(n_steps):
-            run(i)
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b)
+        return timed_on(stream, n_steps, run)
 
     sraw = stream.cuda_stream
     for i in range(args.warmup):
@@ -290,15 +481,7 @@ def main():
     ms = graph_ms if use_graph else eager_ms
 
     # pass B: per-kernel HIP events (eager launches on the same stream)
-    foe.profile_reset()
-    foe.profile_enable(True)
-    t_b = timed(args.steps, lambda i: step(i, sraw))
-    foe.profile_enable(False)
-    kernels = {}
-    for name in foe.profile_names():
-        n, tot = foe.profile_kernel(name)
-        kernels[name] = {"launches": n, "avg_us": round(tot / n * 1e3, 3), "total_ms": tot}
-    foe.profile_reset()
+    t_b, kernels = kernel_profile(foe, args.steps, lambda n: timed(n, lambda i: step(i, sraw)))
     dom = max(kernels, key=lambda n: kernels[n]["total_ms"])
     roof = roofline(dom, cfg, e_touched, kernels[dom]["avg_us"] * 1e-6)
     roof["traffic"] = measured_traffic(args.config, dom)

@@ -5,22 +5,13 @@
 // averaged over the groups:
 //   r[h, i]    = x[h, i] + Attn_h(x[h, :])[i]
 //   r_full[i]  = (1/H) sum_h r[h, i]
-// Five launches: the q/k/v projection of every group (one grouped GEMM with a
-// segment per group), the rotary embedding of q and k in place, the
-// attention, the output projection (grouped GEMM), and the residual average.
-//
-// Attention (head dim 128): a workgroup owns 64 queries of NH query heads of
-// one group (4 waves per head, 16 queries per wave) and walks the key blocks
-// of 64 up to its diagonal.  Per block the keys go to LDS as rows [key][dim]
-// and the values transposed as rows [dim][key], both with XOR-swizzled
-// 16/8-byte chunks; the next block is prefetched into registers meanwhile.  A
-// wave computes the score tile transposed, S^T = K Q^T, on
-// v_mfma_f32_16x16x32_bf16: lane l then holds 16 scores of query l%16, so the
-// online softmax (exp2 form) needs only a reduction over the four lane groups
-// and the probabilities are already laid out as the B operand of
-// O^T += V^T P^T.  Keys of the MFMA K dimension follow the order the score
-// registers come in; the transposed value tile is read in that same order.
+// Launches: the q/k/v projection of every group (one grouped GEMM with a
+// segment per group), a preparation pass (rotary embedding of q and k in
+// place, value head transposed), the attention, the output projection
+// (grouped GEMM), and the residual average.  The kernels below describe their
+// layouts.
 #include "foe_common.hpp"
+#include "lds_dma.hpp"
 
 namespace foe {
 namespace {
@@ -29,191 +20,262 @@ constexpr int kHd = 128;  // head dimension the attention kernel is built for
 constexpr int kQB = 64;   // queries per workgroup and head
 constexpr int kKB = 64;   // keys per block
 
-// ---- rotary embedding -------------------------------------------------------
-// One wave per (row, head) of the q and k heads; lane i rotates the pair
-// (i, i + 64) by the angle (s / scale) * theta^(-2i/128).  The angle is formed
-// and reduced modulo 2*pi in double, then sin/cos in float.
-__global__ __launch_bounds__(256) void rope_kernel(bf16* __restrict__ qkv, int rows, int S,
-                                                   int nq, double theta, double scale) {
-  const int lane = lane_id();
-  const long long wid = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int nh = nq + 1;  // q heads and the k head
-  if (wid >= (long long)rows * nh) return;
-  const int row = (int)(wid / nh), head = (int)(wid % nh);
-  const int s = row % S;
+// ---- preparation pass ----------------------------------------------------------
+// One workgroup per (64-row block, group).  (1) Rotary embedding of the q and
+// k heads in place: thread (row, i) forms the angle (s / scale) *
+// theta^(-2i/128) once, in double, reduced modulo 2*pi, and rotates the pair
+// (i, i + 64) of every q head and of the k head.  (2) The value head
+// transposed to vt[group][dim][key] (keys padded to s_pad with zeros), with
+// the keys of each 16-key group stored in the order 0-3, 8-11, 4-7, 12-15
+// (bits 2 and 3 swapped): that is the key order of the probabilities a lane
+// holds as its B operand, so one 16-byte read gives its V^T operand.
+__device__ __forceinline__ int vt_perm(int key) {
+  return (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
+}
+
+__global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16* __restrict__ vt,
+                                                   int S, int s_pad, int nq, double theta,
+                                                   double scale) {
+  __shared__ double inv_freq[kHd / 2];
+  __shared__ __align__(16) bf16 vtile[kHd][kKB + 8];  // 144-byte rows
+  const int tid = threadIdx.x;
+  const int blk = blockIdx.x, grp = blockIdx.y;
   const size_t ld = (size_t)(nq + 2) * kHd;
-  bf16* v = qkv + (size_t)row * ld + (size_t)head * kHd;
-  const double inv_freq = pow(theta, -2.0 * lane / kHd);
-  double a = (double)s / scale * inv_freq;
+  bf16* base = qkv + (size_t)grp * S * ld;
+  if (tid < kHd / 2) inv_freq[tid] = pow(theta, -2.0 * tid / kHd);
+  __syncthreads();
+
+  const int i = tid & 63;
+  const double f = inv_freq[i];
   constexpr double kTwoPi = 6.283185307179586476925286766559;
-  a -= kTwoPi * floor(a / kTwoPi);
-  float sn, cs;
-  sincosf((float)a, &sn, &cs);
-  const float x1 = (float)v[lane], x2 = (float)v[lane + kHd / 2];
-  v[lane] = (bf16)(x1 * cs - x2 * sn);
-  v[lane + kHd / 2] = (bf16)(x2 * cs + x1 * sn);
+  for (int j = 0; j < kQB / 4; ++j) {
+    const int s = blk * kQB + (tid >> 6) + 4 * j;
+    if (s >= S) break;
+    double a = (double)s / scale * f;
+    a -= kTwoPi * floor(a / kTwoPi);
+    float sn, cs;
+    sincosf((float)a, &sn, &cs);
+    bf16* row = base + (size_t)s * ld;
+    for (int h = 0; h <= nq; ++h) {
+      bf16* v = row + (size_t)h * kHd;
+      const float x1 = (float)v[i], x2 = (float)v[i + kHd / 2];
+      v[i] = (bf16)(x1 * cs - x2 * sn);
+      v[i + kHd / 2] = (bf16)(x2 * cs + x1 * sn);
+    }
+  }
+
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const int p = tid + 256 * m;
+    const int kl = p >> 4, c = p & 15;
+    const int s = blk * kKB + kl;
+    const bf16x8 v = s < S ? *reinterpret_cast<const bf16x8*>(base + (size_t)s * ld +
+                                                              (size_t)(nq + 1) * kHd + c * 8)
+                           : bf16x8{};
+    const int pk = vt_perm(kl);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) vtile[c * 8 + e][pk] = v[e];
+  }
+  __syncthreads();
+  bf16* dst = vt + (size_t)grp * kHd * s_pad + (size_t)blk * kKB;
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const int p = tid + 256 * m;
+    const int dim = p >> 3, c = p & 7;
+    *reinterpret_cast<bf16x8*>(dst + (size_t)dim * s_pad + c * 8) =
+        *reinterpret_cast<const bf16x8*>(&vtile[dim][c * 8]);
+  }
 }
 
 // ---- attention ----------------------------------------------------------------
-// K tile: key r, dims [8c, 8c+8) in 16-byte chunk c ^ (r & 15) of row r (256 B).
-// V^T tile: dim r, keys [4c, 4c+4) in 8-byte chunk c ^ (r & 15) of row r (128 B).
-__device__ __forceinline__ int k_off(int r, int c) { return r * 256 + ((c ^ (r & 15)) << 4); }
-__device__ __forceinline__ int vt_off(int r, int key) {
-  return r * 128 + ((((key >> 2) ^ (r & 15))) << 3) + ((key & 3) << 1);
-}
-
+// Workgroup: 64 queries of NH query heads of one group (the heads share the
+// group's key/value head, so they share its LDS tiles); wave w holds 32
+// queries of head w/2.  Key blocks of 64 go through a 2-stage LDS ring filled
+// by LDS-DMA while the previous block is used:
+//   K tile   [64 keys][128 dims], 256-byte rows, 16-byte chunk c in slot
+//            c ^ (key & 15);
+//   V^T tile [128 dims][64 keys], 128-byte rows, chunk c in slot c ^ swz8(dim).
+// Scores come out transposed, S^T = K Q^T (v_mfma_f32_32x32x16_bf16, A = K
+// rows, B = Q^T held in registers): lane l holds 32 scores of query l%32, at
+// keys 32t + 8(v/4) + 4(l/32) + v%4 of tile t.  Its 8 scores of key step u
+// (16 keys) are directly the B operand of O^T += V^T P^T, whose A operand
+// reads the V^T tile in the same key order (the permuted layout written by
+// the preparation pass).
+// Online softmax in base 2 with a lazily updated maximum: the running maximum
+// m moves only when a block's maximum exceeds it by more than 8 (units of
+// log2), so probabilities stay below 2^8 and the accumulators are rescaled
+// only on those (wave-uniform) steps; the final O / l cancels m exactly.
+// Masking (causal, and keys past S) runs only on the blocks that need it.
+// Causal balance: the workgroups of the first half take query blocks from the
+// last one down and those of the second half from the first one up, so two
+// workgroups that share a compute unit tend to sum to one full walk.
 template <int NH>
-__global__ __launch_bounds__(NH * 256) void attn_kernel(const bf16* __restrict__ qkv, int S,
-                                                        int nq, float scale_log2,
-                                                        bf16* __restrict__ out) {
-  __shared__ __align__(16) unsigned char ks[kKB * kHd * 2];
-  __shared__ __align__(16) unsigned char vts[kHd * kKB * 2];
+__global__ __launch_bounds__(NH * 128) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(const bf16* __restrict__ qkv,
+                                                            const bf16* __restrict__ vt, int S,
+                                                            int s_pad, int nq, int H,
+                                                            float c_log2, bf16* __restrict__ out) {
+  constexpr int NW = 2 * NH;            // waves
+  constexpr int KT = kKB * kHd * 2;     // K tile bytes
+  constexpr int VT = kHd * kKB * 2;     // V^T tile bytes
+  constexpr int STAGE = KT + VT;
+  constexpr int KI = KT / 1024 / NW;    // DMA instructions per wave and tile
+  constexpr int VI = VT / 1024 / NW;
+  __shared__ __align__(1024) unsigned char smem[2 * STAGE];
+
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid >> 6;
-  const int hw = wave & 3;   // wave within its head
-  const int hh = wave >> 2;  // head within the workgroup
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int nqb = (S + kQB - 1) / kQB;
-  const int qb = nqb - 1 - (int)blockIdx.x;  // longest causal walks first
-  const int head = blockIdx.y * NH + hh;
-  const int grp = blockIdx.z;
+  const int hgs = nq / NH;
+  const int P = hgs * H;
+  const int half = (nqb + 1) / 2 * P;
+  const int r = blockIdx.x;
+  const int qb = r < half ? nqb - 1 - r / P : (r - half) / P;
+  const int rest = r < half ? r % P : (r - half) % P;
+  const int grp = rest / hgs;
+  const int head = (rest % hgs) * NH + (wave >> 1);
   const size_t ld = (size_t)(nq + 2) * kHd;
-  const bf16* base = qkv + (size_t)grp * S * ld;
-  const int q0 = qb * kQB + hw * 16;  // this wave's first query
-  const int qi = lane & 15, g = lane >> 4;
-  const int qabs = q0 + qi;
+  const bf16* gbase = qkv + (size_t)grp * S * ld;
+  const int q0 = qb * kQB + (wave & 1) * 32;  // this wave's first query
+  const int qi = lane & 31, hl = lane >> 5;
+  const int q = q0 + qi;
 
-  // Q fragments (B operand of S^T = K Q^T): query qi, dims kk*32 + 8g .. +8
-  bf16x8 qf[4];
+  // Q^T fragments: query q, dims 16 st + 8 hl + [0, 8)
+  bf16x8 qf[8];
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-    if (qabs < S && head < nq)
-      qf[kk] = *reinterpret_cast<const bf16x8*>(base + (size_t)qabs * ld + (size_t)head * kHd +
-                                                kk * 32 + 8 * g);
-    else
-      qf[kk] = bf16x8{};
+  for (int st = 0; st < 8; ++st)
+    qf[st] = q < S ? *reinterpret_cast<const bf16x8*>(gbase + (size_t)q * ld +
+                                                      (size_t)head * kHd + st * 16 + hl * 8)
+                   : bf16x8{};
+
+  // DMA: K instruction g = wave*KI + i fills key rows 4g .. 4g+3 (lane ->
+  // row 4g + lane/16, slot lane%16); V^T instruction g fills dim rows 8g ..
+  // 8g+7 (lane -> row 8g + lane/8, slot lane%8).  Keys past S read zeros
+  // (the K range ends at the group's last row; V^T is zero-padded).
+  const __amdgpu_buffer_rsrc_t rk =
+      make_rsrc_u(gbase + (size_t)nq * kHd, (uint32_t)(((size_t)S * ld - (size_t)nq * kHd) * 2));
+  const __amdgpu_buffer_rsrc_t rv =
+      make_rsrc_u(vt + (size_t)grp * kHd * s_pad, (uint32_t)((size_t)kHd * s_pad * 2));
+  uint32_t koff[KI], voff[VI];
+#pragma unroll
+  for (int i = 0; i < KI; ++i) {
+    const int row = 4 * (wave * KI + i) + (lane >> 4);
+    koff[i] = (uint32_t)((size_t)row * ld * 2) + (uint32_t)((((lane & 15) ^ (row & 15))) << 4);
   }
-
-  f32x4 oacc[8];
 #pragma unroll
-  for (int t = 0; t < 8; ++t) oacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -__builtin_inff();  // running max of this lane's query (log2 units)
+  for (int i = 0; i < VI; ++i) {
+    const int row = 8 * (wave * VI + i) + (lane >> 3);
+    voff[i] = (uint32_t)row * s_pad * 2u + (uint32_t)(((lane & 7) ^ swz<8>(row)) << 4);
+  }
+  const uint32_t sbase = lds_addr(smem);
+  auto issue = [&](int kb) {
+    const uint32_t st = sbase + (uint32_t)(kb & 1) * STAGE;
+    const uint32_t kstep = (uint32_t)kb * kKB * (uint32_t)ld * 2u;
+    const uint32_t lk = st + (uint32_t)wave_u * KI * 1024;
+    const uint32_t lv = st + KT + (uint32_t)wave_u * VI * 1024;
+#pragma unroll
+    for (int i = 0; i < KI; ++i) dma16(rk, koff[i] + kstep, lk, i * 1024);
+#pragma unroll
+    for (int i = 0; i < VI; ++i) dma16(rv, voff[i] + (uint32_t)kb * kKB * 2u, lv, i * 1024);
+  };
+
+  f32x16 oacc[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) oacc[t][v] = 0.f;
+  float m_run = -__builtin_inff();  // running maximum of query q, scaled (log2 units)
   float l_run = 0.f;                // this lane's share of the running sum
 
-  // block loads: 64 keys x 128 dims of K and of V, 16 bytes per piece; thread
-  // t handles pieces t, t + NT, ... (key = piece / 16, dims (piece % 16) * 8)
-  constexpr int NT = NH * 256;
-  constexpr int NPC = kKB * kHd / 8 / NT;  // pieces of K (and of V) per thread
-  bf16x8 kreg[NPC], vreg[NPC];
-  auto load_block = [&](int kb) {
-#pragma unroll
-    for (int i = 0; i < NPC; ++i) {
-      const int pc = tid + i * NT;
-      const int key = kb * kKB + (pc >> 4), c = pc & 15;
-      if (key < S) {
-        const bf16* row = base + (size_t)key * ld + (size_t)nq * kHd;
-        kreg[i] = *reinterpret_cast<const bf16x8*>(row + c * 8);
-        vreg[i] = *reinterpret_cast<const bf16x8*>(row + kHd + c * 8);
-      } else {
-        kreg[i] = bf16x8{};
-        vreg[i] = bf16x8{};
-      }
-    }
-  };
-  auto store_block = [&]() {
-#pragma unroll
-    for (int i = 0; i < NPC; ++i) {
-      const int pc = tid + i * NT;
-      const int key = pc >> 4, c = pc & 15;
-      *reinterpret_cast<bf16x8*>(ks + k_off(key, c)) = kreg[i];
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        *reinterpret_cast<bf16*>(vts + vt_off(c * 8 + e, key)) = vreg[i][e];
-    }
-  };
-
   const int nkb = min(qb + 1, (S + kKB - 1) / kKB);
-  load_block(0);
+  issue(0);
   for (int kb = 0; kb < nkb; ++kb) {
-    __syncthreads();  // the previous block's tiles are no longer read
-    store_block();
-    __syncthreads();
-    if (kb + 1 < nkb) load_block(kb + 1);
+    // block kb has landed for every wave, and every wave is done with kb - 1
+    vm_barrier<0>();
+    if (kb + 1 < nkb) issue(kb + 1);
+    const unsigned char* ks = smem + (kb & 1) * STAGE;
+    const unsigned char* vs = ks + KT;
 
-    // scores S^T[key][query]: lane holds keys kb*64 + 16j + 4g + v of query qi
-    f32x4 sacc[4];
+    f32x16 sacc[2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      sacc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int kr = j * 16 + qi;  // key row of this lane's A fragment
+    for (int t = 0; t < 2; ++t) {
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + k_off(kr, kk * 4 + g));
-        sacc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kk], sacc[j], 0, 0, 0);
+      for (int v = 0; v < 16; ++v) sacc[t][v] = 0.f;
+      const int row = t * 32 + qi;
+#pragma unroll
+      for (int st = 0; st < 8; ++st) {
+        const bf16x8 kf =
+            *reinterpret_cast<const bf16x8*>(ks + row * 256 + (((st * 2 + hl) ^ (row & 15)) << 4));
+        sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st], sacc[t], 0, 0, 0);
       }
     }
-    // mask (causal and past the sequence), scale, running max
-    float mx = -__builtin_inff();
+    const int kbase = kb * kKB;
+    if (kbase + kKB - 1 > q0 || kbase + kKB > S) {  // wave-uniform
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int key = kb * kKB + j * 16 + 4 * g + v;
-        const float sv = (key <= qabs && key < S) ? sacc[j][v] * scale_log2 : -__builtin_inff();
-        sacc[j][v] = sv;
-        mx = fmaxf(mx, sv);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
+        for (int v = 0; v < 16; ++v) {
+          const int key = kbase + t * 32 + (v >> 2) * 8 + hl * 4 + (v & 3);
+          if (key > q || key >= S) sacc[t][v] = -__builtin_inff();
+        }
+    }
+    float mx = sacc[0][0];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[t][v]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    // a query with no visible key yet keeps m = -inf: scale 1, probabilities 0
-    const bool live = m_new != -__builtin_inff();
-    const float alpha = live ? exp2f(m_run - m_new) : 1.f;
-    float psum = 0.f;
-    bf16x8 pf[2];
+    const float mxs = mx * c_log2;
+    // every query sees key 0 (or, past S, keys below S) in block 0, so mxs is
+    // finite and the first block always moves m
+    const bool need = mxs > m_run + 8.f;
+    if (__builtin_amdgcn_ballot_w64(need) != 0) {
+      const float alpha = need ? __builtin_amdgcn_exp2f(m_run - mxs) : 1.f;
+      if (need) m_run = mxs;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+      for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float p = live ? exp2f(sacc[j][v] - m_new) : 0.f;
-        psum += p;
-        pf[j >> 1][(j & 1) * 4 + v] = (bf16)p;
+        for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
+      l_run *= alpha;
+    }
+    bf16x8 pf[4];
+    float ps = 0.f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[t][v], c_log2, -m_run));
+        ps += p;
+        pf[t * 2 + (v >> 3)][v & 7] = (bf16)p;
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
+    l_run += ps;
 #pragma unroll
-    for (int t = 0; t < 8; ++t)
+    for (int dt = 0; dt < 4; ++dt) {
+      const int row = dt * 32 + qi;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) oacc[t][v] *= alpha;
-    // O^T[dim][query] += V^T[dim][keys] P^T[keys][query]; k-slot group g of
-    // step s holds keys 32s + 4g + [0,4) and 32s + 16 + 4g + [0,4)
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const int r = t * 16 + qi;  // dim row of this lane's A fragment
-        const uint2 lo = *reinterpret_cast<const uint2*>(vts + vt_off(r, 32 * s2 + 4 * g));
-        const uint2 hi = *reinterpret_cast<const uint2*>(vts + vt_off(r, 32 * s2 + 16 + 4 * g));
-        const uint4 vv = uint4{lo.x, lo.y, hi.x, hi.y};
-        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vv),
-                                                          pf[s2], oacc[t], 0, 0, 0);
+      for (int u = 0; u < 4; ++u) {
+        const bf16x8 vf =
+            *reinterpret_cast<const bf16x8*>(vs + row * 128 + (((u * 2 + hl) ^ swz<8>(row)) << 4));
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[u], oacc[dt], 0, 0, 0);
       }
     }
   }
 
-  // O[query][dim] = O^T / l; lane holds dims 16t + 4g + [0,4) of query qi
-  float l = l_run + __shfl_xor(l_run, 16);
-  l += __shfl_xor(l, 32);
-  if (qabs < S && head < nq) {
+  // O[q][dim] = O^T / l; lane holds dims 32 dt + 8 g + 4 hl + [0, 4)
+  const float l = l_run + __shfl_xor(l_run, 32);
+  if (q < S) {
     const float inv = 1.f / l;
-    bf16* orow = out + ((size_t)grp * S + qabs) * ((size_t)nq * kHd) + (size_t)head * kHd;
+    bf16* orow = out + ((size_t)grp * S + q) * ((size_t)nq * kHd) + (size_t)head * kHd;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      bf16x4 o;
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) o[v] = (bf16)(oacc[t][v] * inv);
-      *reinterpret_cast<bf16x4*>(orow + t * 16 + 4 * g) = o;
-    }
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 o;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) o[v] = (bf16)(oacc[dt][g * 4 + v] * inv);
+        *reinterpret_cast<bf16x4*>(orow + dt * 32 + g * 8 + hl * 4) = o;
+      }
   }
 }
 
@@ -249,7 +311,7 @@ __global__ void iota_kernel(int32_t* p, int n, int step) {
 }
 
 struct AttnWs {
-  size_t offsets, qkv, o, a, total;
+  size_t offsets, qkv, vt, o, a, total;
 };
 
 AttnWs attn_ws(int H, int S, int d, int nq, int hd) {
@@ -263,6 +325,7 @@ AttnWs attn_ws(int H, int S, int d, int nq, int hd) {
   };
   take(w.offsets, (size_t)(H + 1) * 4);
   take(w.qkv, rows * (nq + 2) * hd * 2);
+  take(w.vt, (size_t)H * hd * ceil_div(S, kKB) * kKB * 2);
   take(w.o, rows * nq * hd * 2);
   take(w.a, rows * d * 2);
   w.total = align_up(off, 256);
@@ -293,20 +356,23 @@ hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float the
   hipError_t e = launch_grouped_gemm(x, offsets, H, rows, w_qkv, (nq + 2) * hd, d, qkv, s,
                                      "attn_qkv");
   if (e != hipSuccess) return e;
+  bf16* vt = reinterpret_cast<bf16*>(base + L.vt);
+  const int nqb = ceil_div(S, kQB);
+  const int s_pad = nqb * kKB;
   {
-    ProfileScope ps("attn_rope", s);
-    FOE_LAUNCH(rope_kernel, dim3(ceil_div((long long)rows * (nq + 1), 4)), dim3(256), 0, s, qkv,
-               rows, S, nq, (double)theta, (double)scale);
+    ProfileScope ps("attn_prep", s);
+    FOE_LAUNCH(prep_kernel, dim3(nqb, H), dim3(256), 0, s, qkv, vt, S, s_pad, nq, (double)theta,
+               (double)scale);
   }
   {
     ProfileScope ps("attn_core", s);
-    const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
-    const int nqb = ceil_div(S, kQB);
+    const float c_log2 = 1.4426950408889634f / sqrtf((float)hd);
     if (nq % 2 == 0)
-      FOE_LAUNCH(attn_kernel<2>, dim3(nqb, nq / 2, H), dim3(512), 0, s, qkv, S, nq, scale_log2,
-                 o);
+      FOE_LAUNCH(attn_fwd_kernel<2>, dim3(nqb * (nq / 2) * H), dim3(256), 0, s, qkv, vt, S, s_pad,
+                 nq, H, c_log2, o);
     else
-      FOE_LAUNCH(attn_kernel<1>, dim3(nqb, nq, H), dim3(256), 0, s, qkv, S, nq, scale_log2, o);
+      FOE_LAUNCH(attn_fwd_kernel<1>, dim3(nqb * nq * H), dim3(128), 0, s, qkv, vt, S, s_pad, nq,
+                 H, c_log2, o);
   }
   e = launch_grouped_gemm(o, offsets, H, rows, w_o, d, nq * hd, a, s, "attn_out");
   if (e != hipSuccess) return e;
