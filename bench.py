@@ -73,7 +73,7 @@ KERNEL_SOURCES = {"route": "route.hip", "permute_index": "permute.hip",
                   "ffn_gateup": "ffn.hip", "ffn_down": "ffn.hip", "ffn_gateup_f32": "ffn.hip",
                   "ffn_down_f32": "ffn.hip", "combine": "combine.hip", "reduce": "combine.hip",
                   "attn_qkv": "ffn.hip", "attn_out": "ffn.hip", "attn_prep": "attention.hip",
-                  "attn_core": "attention.hip", "attn_resid_avg": "attention.hip"}
+                  "attn_core": "attention.hip"}
 
 
 def source_sha(kernel):
@@ -157,9 +157,10 @@ def attention_work(name, cfg):
         return (4.0 * hd * nq * H * S * (S + 1) / 2,
                 2.0 * (rows * n_qkv + rows * nq * hd))
     if name == "attn_out":
-        return 2.0 * rows * nq * hd * d, 2.0 * (rows * nq * hd + H * d * nq * hd + rows * d)
-    if name == "attn_resid_avg":
-        return 0.0, 2.0 * (2 * rows * d + S * d)
+        # one product over the concatenated head outputs plus the residual
+        # planes: o, w_o and x read once, r_full written once
+        return (2.0 * rows * nq * hd * d,
+                2.0 * (rows * nq * hd + H * d * nq * hd + rows * d + S * d))
     return 0.0, 0.0
 
 
@@ -293,7 +294,7 @@ def main_attention(args):
 
     x = up(inp["x"])
     w_qkv = up(np.stack([g["w_qkv"] for g in inp["groups"]]))
-    w_o = up(np.stack([g["w_o"] for g in inp["groups"]]))
+    w_o = up(np.concatenate([g["w_o"] for g in inp["groups"]], axis=1))
     out = torch.empty((S, d), dtype=torch.bfloat16, device=dev)
     L = foe.lib()
     ws_n = L.foe_group_attention_workspace_bytes(H, S, d, nq, hd)

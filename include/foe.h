@@ -233,7 +233,10 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
  * foe_group_attention - the per-group attention that feeds the block (Table 3,
  * FoE column, rows "Attn. residual" and "Cross-group avg."):
  *   r[h,i]    = x[h,i] + Attn_h(x[h,:])[i]     (every group its own representation)
- *   r_full[i] = (1/H) sum_h r[h,i]             (fp32, h = 0..H-1 in order)
+ *   r_full[i] = (1/H) sum_h r[h,i]
+ * computed as (1/H) (sum_h o[h,i] w_o[h]^T + sum_h x[h,i]) in fp32: the output
+ * projections of all groups form one product over the concatenated head
+ * outputs, and the residuals are added after it (h = 0..H-1 in order).
  * Attn_h: causal self-attention over the S tokens (positions 0..S-1) with one
  * key/value head and nq query heads sharing it (grouped-query attention),
  * scores q.k/sqrt(hd), rotary embedding on q and k pairing dimension i with
@@ -241,12 +244,15 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
  *
  *   x        [H,S,d]          bf16
  *   w_qkv    [H,(nq+2)*hd,d]  bf16  rows: nq query heads, the key head, the value head
- *   w_o      [H,d,nq*hd]      bf16
+ *   w_o      [d,H*nq*hd]      bf16  the groups' output projections side by side:
+ *                                   columns h*nq*hd .. (h+1)*nq*hd-1 belong to group h
  *   theta    rotary base (> 0);  scale: rotary scaling factor (> 0), positions / scale
  *   r_full   [S,d]            bf16 out
  *   ws, ws_bytes              workspace of foe_group_attention_workspace_bytes()
- * bf16 only and hd = 128 (else FOE_ERR_UNSUPPORTED); H*S*d, H*S*(nq+2)*hd below
- * 2^30 elements.
+ * All pointers are device memory owned by the caller, 16-byte aligned (the
+ * workspace too); the call enqueues work on `stream` and returns.  bf16 only
+ * and hd = 128 (else FOE_ERR_UNSUPPORTED); H*S*d and H*S*(nq+2)*hd must stay
+ * below 2^30 elements.  S = 0 is a no-op.
  */
 int foe_group_attention(foe_dtype dt, int H, int S, int d, int nq, int hd, float theta,
                         float scale, const void* x, const void* w_qkv, const void* w_o,

@@ -7,9 +7,10 @@
 //   r_full[i]  = (1/H) sum_h r[h, i]
 // Launches: the q/k/v projection of every group (one grouped GEMM with a
 // segment per group), a preparation pass (rotary embedding of q and k in
-// place, value head transposed), the attention, the output projection
-// (grouped GEMM), and the residual average.  The kernels below describe their
-// layouts.
+// place, value head transposed), the attention (o as [S][H*nq*hd]), and the
+// output projection of all groups as one GEMM over K = H*nq*hd whose epilogue
+// adds sum_h x[h] and scales by 1/H, so the per-group outputs never reach
+// memory.  The kernels below describe their layouts.
 #include "foe_common.hpp"
 #include "lds_dma.hpp"
 
@@ -88,10 +89,17 @@ __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16*
 }
 
 // ---- attention ----------------------------------------------------------------
-// Workgroup: 64 queries of NH query heads of one group (the heads share the
-// group's key/value head, so they share its LDS tiles); wave w holds 32
-// queries of head w/2.  Key blocks of 64 go through a 2-stage LDS ring filled
-// by LDS-DMA while the previous block is used:
+// Task: 64 queries of NH query heads of one group (the heads share the
+// group's key/value head and so its LDS tiles).  A workgroup has two halves
+// of 2*NH waves; wave (half, head hh, query half qw) holds 32 queries.  The
+// halves split the task's key blocks of 64 (half 0 the even ones, half 1 the
+// odd ones) and merge their partial softmax states through LDS at the end, so
+// that every running workgroup keeps two waves on each SIMD however short its
+// task.  Tasks are numbered longest first; with one workgroup per compute unit
+// the dispatcher hands the next task to the first unit that frees up, which
+// balances the causal walks.
+// Each half streams its key blocks through its own 2-stage LDS rings filled by
+// LDS-DMA:
 //   K tile   [64 keys][128 dims], 256-byte rows, 16-byte chunk c in slot
 //            c ^ (key & 15);
 //   V^T tile [128 dims][64 keys], 128-byte rows, chunk c in slot c ^ swz8(dim).
@@ -101,55 +109,66 @@ __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16*
 // (16 keys) are directly the B operand of O^T += V^T P^T, whose A operand
 // reads the V^T tile in the same key order (the permuted layout written by
 // the preparation pass).
+// Software pipeline: an iteration computes the scores of its block, then the
+// P V product of the half's previous block while the softmax of the new block
+// runs on the vector ALUs (independent instructions, interleaved); the K ring
+// runs one block ahead, the V ring one block behind.
 // Online softmax in base 2 with a lazily updated maximum: the running maximum
 // m moves only when a block's maximum exceeds it by more than 8 (units of
 // log2), so probabilities stay below 2^8 and the accumulators are rescaled
 // only on those (wave-uniform) steps; the final O / l cancels m exactly.
 // Masking (causal, and keys past S) runs only on the blocks that need it.
-// Causal balance: the workgroups of the first half take query blocks from the
-// last one down and those of the second half from the first one up, so two
-// workgroups that share a compute unit tend to sum to one full walk.
 template <int NH>
-__global__ __launch_bounds__(NH * 128) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(const bf16* __restrict__ qkv,
-                                                            const bf16* __restrict__ vt, int S,
-                                                            int s_pad, int nq, int H,
-                                                            float c_log2, bf16* __restrict__ out) {
-  constexpr int NW = 2 * NH;            // waves
+__global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(
+    const bf16* __restrict__ qkv, const bf16* __restrict__ vt, int S, int s_pad, int nq, int H,
+    float c_log2, bf16* __restrict__ out) {
+  constexpr int HW = 2 * NH;            // waves per half
   constexpr int KT = kKB * kHd * 2;     // K tile bytes
   constexpr int VT = kHd * kKB * 2;     // V^T tile bytes
-  constexpr int STAGE = KT + VT;
-  constexpr int KI = KT / 1024 / NW;    // DMA instructions per wave and tile
-  constexpr int VI = VT / 1024 / NW;
-  __shared__ __align__(1024) unsigned char smem[2 * STAGE];
+  constexpr int HALF = 2 * KT + 2 * VT; // LDS bytes per half
+  constexpr int KI = KT / 1024 / HW;    // DMA instructions per wave and tile
+  constexpr int VI = VT / 1024 / HW;
+  static_assert(HW * 64 * 64 * 4 <= 2 * HALF, "merge buffer fits in the rings");
+  __shared__ __align__(1024) unsigned char smem[2 * HALF];
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid >> 6;
-  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int half = wave / HW;        // key blocks half, half + 2, ...
+  const int hw = wave % HW;          // wave within its half
+  const int hw_u = __builtin_amdgcn_readfirstlane(hw);
+  const int half_u = __builtin_amdgcn_readfirstlane(half);
   const int nqb = (S + kQB - 1) / kQB;
   const int hgs = nq / NH;
   const int P = hgs * H;
-  const int half = (nqb + 1) / 2 * P;
   const int r = blockIdx.x;
-  const int qb = r < half ? nqb - 1 - r / P : (r - half) / P;
-  const int rest = r < half ? r % P : (r - half) % P;
+  const int qb = nqb - 1 - r / P;    // longest walks first
+  const int rest = r % P;
   const int grp = rest / hgs;
-  const int head = (rest % hgs) * NH + (wave >> 1);
+  const int head = (rest % hgs) * NH + (hw >> 1);
   const size_t ld = (size_t)(nq + 2) * kHd;
   const bf16* gbase = qkv + (size_t)grp * S * ld;
-  const int q0 = qb * kQB + (wave & 1) * 32;  // this wave's first query
+  const int q0 = qb * kQB + (hw & 1) * 32;  // this wave's first query
   const int qi = lane & 31, hl = lane >> 5;
   const int q = q0 + qi;
 
   // Q^T fragments: query q, dims 16 st + 8 hl + [0, 8)
   bf16x8 qf[8];
+  {
+    const bf16* qrow = gbase + (size_t)min(q, S - 1) * ld + (size_t)head * kHd + hl * 8;
 #pragma unroll
-  for (int st = 0; st < 8; ++st)
-    qf[st] = q < S ? *reinterpret_cast<const bf16x8*>(gbase + (size_t)q * ld +
-                                                      (size_t)head * kHd + st * 16 + hl * 8)
-                   : bf16x8{};
+    for (int st = 0; st < 8; ++st) {
+      qf[st] = *reinterpret_cast<const bf16x8*>(qrow + st * 16);
+      if (q >= S) qf[st] = bf16x8{};
+    }
+  }
+  // The fragments must have arrived before the loop: the compiler would
+  // otherwise wait for them (vmcnt(0)) inside the loop, which also waits for
+  // the LDS-DMA of the next block issued there.
+#pragma unroll
+  for (int st = 0; st < 8; ++st) asm volatile("" ::"v"(qf[st]));
 
-  // DMA: K instruction g = wave*KI + i fills key rows 4g .. 4g+3 (lane ->
+  // DMA: K instruction g = hw*KI + i fills key rows 4g .. 4g+3 (lane ->
   // row 4g + lane/16, slot lane%16); V^T instruction g fills dim rows 8g ..
   // 8g+7 (lane -> row 8g + lane/8, slot lane%8).  Keys past S read zeros
   // (the K range ends at the group's last row; V^T is zero-padded).
@@ -160,96 +179,31 @@ __global__ __launch_bounds__(NH * 128) __attribute__((amdgpu_waves_per_eu(2, 2))
   uint32_t koff[KI], voff[VI];
 #pragma unroll
   for (int i = 0; i < KI; ++i) {
-    const int row = 4 * (wave * KI + i) + (lane >> 4);
+    const int row = 4 * (hw * KI + i) + (lane >> 4);
     koff[i] = (uint32_t)((size_t)row * ld * 2) + (uint32_t)((((lane & 15) ^ (row & 15))) << 4);
   }
 #pragma unroll
   for (int i = 0; i < VI; ++i) {
-    const int row = 8 * (wave * VI + i) + (lane >> 3);
+    const int row = 8 * (hw * VI + i) + (lane >> 3);
     voff[i] = (uint32_t)row * s_pad * 2u + (uint32_t)(((lane & 7) ^ swz<8>(row)) << 4);
   }
-  const uint32_t sbase = lds_addr(smem);
-  auto issue = [&](int kb) {
-    const uint32_t st = sbase + (uint32_t)(kb & 1) * STAGE;
-    const uint32_t kstep = (uint32_t)kb * kKB * (uint32_t)ld * 2u;
-    const uint32_t lk = st + (uint32_t)wave_u * KI * 1024;
-    const uint32_t lv = st + KT + (uint32_t)wave_u * VI * 1024;
+  unsigned char* hs = smem + half * HALF;  // this half's rings
+  const uint32_t hbase = lds_addr(smem) + (uint32_t)half_u * HALF;
+  // the half's i-th block (key block 2i + half) -> K stage i&1 (bytes
+  // [0, 2 KT)), V^T stage i&1 (bytes [2 KT, 2 KT + 2 VT))
+  auto issue_k = [&](int i) {
+    const uint32_t kstep = (uint32_t)(2 * i + half) * kKB * (uint32_t)ld * 2u;
+    const uint32_t lk = hbase + (uint32_t)(i & 1) * KT + (uint32_t)hw_u * KI * 1024;
 #pragma unroll
-    for (int i = 0; i < KI; ++i) dma16(rk, koff[i] + kstep, lk, i * 1024);
-#pragma unroll
-    for (int i = 0; i < VI; ++i) dma16(rv, voff[i] + (uint32_t)kb * kKB * 2u, lv, i * 1024);
+    for (int j = 0; j < KI; ++j) dma16(rk, koff[j] + kstep, lk, j * 1024);
   };
-
-  f32x16 oacc[4];
+  auto issue_v = [&](int i) {
+    const uint32_t lv = hbase + 2 * KT + (uint32_t)(i & 1) * VT + (uint32_t)hw_u * VI * 1024;
+    const uint32_t vstep = (uint32_t)(2 * i + half) * kKB * 2u;
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) oacc[t][v] = 0.f;
-  float m_run = -__builtin_inff();  // running maximum of query q, scaled (log2 units)
-  float l_run = 0.f;                // this lane's share of the running sum
-
-  const int nkb = min(qb + 1, (S + kKB - 1) / kKB);
-  issue(0);
-  for (int kb = 0; kb < nkb; ++kb) {
-    // block kb has landed for every wave, and every wave is done with kb - 1
-    vm_barrier<0>();
-    if (kb + 1 < nkb) issue(kb + 1);
-    const unsigned char* ks = smem + (kb & 1) * STAGE;
-    const unsigned char* vs = ks + KT;
-
-    f32x16 sacc[2];
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) sacc[t][v] = 0.f;
-      const int row = t * 32 + qi;
-#pragma unroll
-      for (int st = 0; st < 8; ++st) {
-        const bf16x8 kf =
-            *reinterpret_cast<const bf16x8*>(ks + row * 256 + (((st * 2 + hl) ^ (row & 15)) << 4));
-        sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st], sacc[t], 0, 0, 0);
-      }
-    }
-    const int kbase = kb * kKB;
-    if (kbase + kKB - 1 > q0 || kbase + kKB > S) {  // wave-uniform
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = kbase + t * 32 + (v >> 2) * 8 + hl * 4 + (v & 3);
-          if (key > q || key >= S) sacc[t][v] = -__builtin_inff();
-        }
-    }
-    float mx = sacc[0][0];
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[t][v]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mxs = mx * c_log2;
-    // every query sees key 0 (or, past S, keys below S) in block 0, so mxs is
-    // finite and the first block always moves m
-    const bool need = mxs > m_run + 8.f;
-    if (__builtin_amdgcn_ballot_w64(need) != 0) {
-      const float alpha = need ? __builtin_amdgcn_exp2f(m_run - mxs) : 1.f;
-      if (need) m_run = mxs;
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
-      l_run *= alpha;
-    }
-    bf16x8 pf[4];
-    float ps = 0.f;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[t][v], c_log2, -m_run));
-        ps += p;
-        pf[t * 2 + (v >> 3)][v & 7] = (bf16)p;
-      }
-    l_run += ps;
+    for (int j = 0; j < VI; ++j) dma16(rv, voff[j] + vstep, lv, j * 1024);
+  };
+  auto pv = [&](f32x16* oacc, const bf16x8* pf, const unsigned char* vs) {
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
       const int row = dt * 32 + qi;
@@ -260,13 +214,158 @@ __global__ __launch_bounds__(NH * 128) __attribute__((amdgpu_waves_per_eu(2, 2))
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[u], oacc[dt], 0, 0, 0);
       }
     }
+  };
+
+  f32x16 oacc[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) oacc[t][v] = 0.f;
+  float m_run = -__builtin_inff();  // running maximum of query q, scaled (log2 units)
+  float l_run = 0.f;                // this lane's share of the running sum
+  float alpha = 1.f;                // rescale owed to oacc before the next P V
+  bool resc = false;                // (wave-uniform) some lane owes a rescale
+  bf16x8 pf[4];                     // probabilities of the previous block (B operand)
+#pragma unroll
+  for (int u = 0; u < 4; ++u) pf[u] = bf16x8{};
+  // P V steps with P = 0 (the first iteration, and the last one of a half
+  // left without a block) may read a V stage no DMA has filled: zero both
+  // stages of both halves so that they add exact zeros
+  for (int i = tid; i < 4 * (VT / 16); i += NH * 256) {
+    const int h = i / (2 * (VT / 16)), c = i % (2 * (VT / 16));
+    *reinterpret_cast<u32x4*>(smem + h * HALF + 2 * KT + c * 16) = u32x4{0u, 0u, 0u, 0u};
+  }
+
+  const int nkb = min(qb + 1, (S + kKB - 1) / kKB);
+  const int niter = (nkb + 1) / 2;  // both halves run the same iterations
+  if (half < nkb) issue_k(0);
+  for (int it = 0; it < niter; ++it) {
+    const int kb = 2 * it + half;
+    const bool valid = kb < nkb;  // wave-uniform
+    // K of this block and V of the previous one have landed for every wave,
+    // and every wave is done with the previous iteration's stages
+    vm_barrier<0>();
+    if (kb + 2 < nkb) issue_k(it + 1);
+    if (valid) issue_v(it);
+    const unsigned char* ks = hs + (it & 1) * KT;
+    const unsigned char* vs = hs + 2 * KT + ((it + 1) & 1) * VT;  // previous block's V
+
+    f32x16 sacc[2];
+    if (valid) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sacc[t][v] = 0.f;
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const int row = t * 32 + qi;
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
+              ks + row * 256 + (((st * 2 + hl) ^ (row & 15)) << 4));
+          sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st], sacc[t], 0, 0, 0);
+        }
+    }
+    if (resc) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
+    }
+    const int kbase = kb * kKB;
+    if (valid && (kbase + kKB - 1 > q0 || kbase + kKB > S)) {  // wave-uniform
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = kbase + t * 32 + (v >> 2) * 8 + hl * 4 + (v & 3);
+          if (key > q || key >= S) sacc[t][v] = -__builtin_inff();
+        }
+    }
+
+    // O^T += V^T P^T for the previous block (zeros at the first iteration)
+    pv(oacc, pf, vs);
+
+    if (valid) {
+      // softmax of this block
+      float mx = sacc[0][0];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[t][v]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mxs = mx * c_log2;
+      // every row sees a key in its half's first block (half 0: key 0; half
+      // 1, which has blocks only when qb >= 1: key 64, as q >= 64 and
+      // S > 64), so mxs is finite and that first block always moves m
+      const bool need = mxs > m_run + 8.f;
+      const float m_new = need ? mxs : m_run;
+      alpha = need ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
+      m_run = m_new;
+      resc = __builtin_amdgcn_ballot_w64(need) != 0;
+      float ps = 0.f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        bf16x8 p8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          p8[e] = (bf16)__builtin_amdgcn_exp2f(
+              fmaf(sacc[u >> 1][(u & 1) * 8 + e], c_log2, -m_run));
+        pf[u] = p8;
+#pragma unroll
+        for (int e = 0; e < 8; e += 2)
+          ps = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p8[e], p8[e + 1]},
+                                               bf16x2{(bf16)1.f, (bf16)1.f}, ps, false);
+      }
+      l_run = l_run * alpha + ps;
+    } else {
+      resc = false;
+      alpha = 1.f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) pf[u] = bf16x8{};
+    }
+  }
+  // the last block's P V (P = 0 if the half's last iteration had no block)
+  vm_barrier<0>();
+  if (resc) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
+  }
+  pv(oacc, pf, hs + 2 * KT + ((niter + 1) & 1) * VT);
+
+  // merge: half 1 hands (m, l, O) to its partner wave of half 0 through LDS
+  // (the rings are free after this barrier)
+  float l = l_run + __shfl_xor(l_run, 32);
+  __syncthreads();
+  float* mb = reinterpret_cast<float*>(smem) + (size_t)hw * (64 * 66);
+  if (half == 1) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mb[(t * 16 + v) * 64 + lane] = oacc[t][v];
+    mb[64 * 64 + lane] = m_run;
+    mb[65 * 64 + lane] = l;
+  }
+  __syncthreads();
+  if (half == 1) return;
+  {
+    const float mo = mb[64 * 64 + lane], lo = mb[65 * 64 + lane];
+    const float m = fmaxf(m_run, mo);
+    const float a0 = m_run == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(m_run - m);
+    const float a1 = mo == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(mo - m);
+    l = l * a0 + lo * a1;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) oacc[t][v] = oacc[t][v] * a0 + mb[(t * 16 + v) * 64 + lane] * a1;
   }
 
   // O[q][dim] = O^T / l; lane holds dims 32 dt + 8 g + 4 hl + [0, 4)
-  const float l = l_run + __shfl_xor(l_run, 32);
   if (q < S) {
     const float inv = 1.f / l;
-    bf16* orow = out + ((size_t)grp * S + q) * ((size_t)nq * kHd) + (size_t)head * kHd;
+    bf16* orow = out + ((size_t)q * H + grp) * ((size_t)nq * kHd) + (size_t)head * kHd;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -279,39 +378,13 @@ __global__ __launch_bounds__(NH * 128) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
 }
 
-// ---- residual average ---------------------------------------------------------
-// r_full = (1/H) sum_h (x[h] + a[h]) in fp32, h = 0..H-1 in order; 8 elements
-// per thread per grid-stride step.
-__global__ __launch_bounds__(256) void resid_avg_kernel(const bf16* __restrict__ x,
-                                                        const bf16* __restrict__ a, int H,
-                                                        long long plane, float inv_h,
-                                                        bf16* __restrict__ out) {
-  const long long nvec = plane / 8;
-  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < nvec;
-       i += (long long)gridDim.x * blockDim.x) {
-    float acc[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-    for (int h = 0; h < H; ++h) {
-      const bf16x8 xv = *reinterpret_cast<const bf16x8*>(x + (size_t)h * plane + i * 8);
-      const bf16x8 av = *reinterpret_cast<const bf16x8*>(a + (size_t)h * plane + i * 8);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += (float)xv[e] + (float)av[e];
-    }
-    bf16x8 o;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = (bf16)(acc[e] * inv_h);
-    *reinterpret_cast<bf16x8*>(out + i * 8) = o;
-  }
-}
-
 __global__ void iota_kernel(int32_t* p, int n, int step) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = i * step;
 }
 
 struct AttnWs {
-  size_t offsets, qkv, vt, o, a, total;
+  size_t offsets, qkv, vt, o, total;
 };
 
 AttnWs attn_ws(int H, int S, int d, int nq, int hd) {
@@ -327,7 +400,6 @@ AttnWs attn_ws(int H, int S, int d, int nq, int hd) {
   take(w.qkv, rows * (nq + 2) * hd * 2);
   take(w.vt, (size_t)H * hd * ceil_div(S, kKB) * kKB * 2);
   take(w.o, rows * nq * hd * 2);
-  take(w.a, rows * d * 2);
   w.total = align_up(off, 256);
   return w;
 }
@@ -347,7 +419,6 @@ hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float the
   int32_t* offsets = reinterpret_cast<int32_t*>(base + L.offsets);
   bf16* qkv = reinterpret_cast<bf16*>(base + L.qkv);
   bf16* o = reinterpret_cast<bf16*>(base + L.o);
-  bf16* a = reinterpret_cast<bf16*>(base + L.a);
   const int rows = H * S;
   {
     ProfileScope ps("attn_offsets", s);
@@ -368,22 +439,18 @@ hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float the
     ProfileScope ps("attn_core", s);
     const float c_log2 = 1.4426950408889634f / sqrtf((float)hd);
     if (nq % 2 == 0)
-      FOE_LAUNCH(attn_fwd_kernel<2>, dim3(nqb * (nq / 2) * H), dim3(256), 0, s, qkv, vt, S, s_pad,
+      FOE_LAUNCH(attn_fwd_kernel<2>, dim3(nqb * (nq / 2) * H), dim3(512), 0, s, qkv, vt, S, s_pad,
                  nq, H, c_log2, o);
     else
-      FOE_LAUNCH(attn_fwd_kernel<1>, dim3(nqb * nq * H), dim3(128), 0, s, qkv, vt, S, s_pad, nq,
+      FOE_LAUNCH(attn_fwd_kernel<1>, dim3(nqb * nq * H), dim3(256), 0, s, qkv, vt, S, s_pad, nq,
                  H, c_log2, o);
   }
-  e = launch_grouped_gemm(o, offsets, H, rows, w_o, d, nq * hd, a, s, "attn_out");
+  // output projection of all groups at once (o is [S][H*nq*hd], w_o
+  // [d][H*nq*hd]) with the residual average in its epilogue:
+  // r_full = (o w_o^T + sum_h x[h]) / H; offsets[0..1] = {0, S}
+  e = launch_gemm_resid(o, offsets, S, w_o, d, H * nq * hd, x, H, (long long)S * d, 1.0f / H,
+                        r_full, s, "attn_out");
   if (e != hipSuccess) return e;
-  {
-    ProfileScope ps("attn_resid_avg", s);
-    const long long plane = (long long)S * d;
-    const long long nvec = plane / 8;
-    const long long want = (nvec + 255) / 256;
-    FOE_LAUNCH(resid_avg_kernel, dim3((unsigned)(want < 8192 ? want : 8192)), dim3(256), 0, s,
-               static_cast<const bf16*>(x), a, H, plane, 1.0f / H, static_cast<bf16*>(r_full));
-  }
   return hipGetLastError();
 }
 

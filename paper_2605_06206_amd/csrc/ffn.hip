@@ -31,6 +31,10 @@
 #ifndef FOE_DMA_DN
 #define FOE_DMA_DN 256, 256, 2, 4, 64, 2, 4, 4, 1
 #endif
+// plain GEMM with the residual epilogue (few M rows: 128 x 256 tiles)
+#ifndef FOE_DMA_RES
+#define FOE_DMA_RES 128, 256, 2, 4, 64, 2, 3, 4, 1
+#endif
 // few rows per expert (decode): LDS-staged weight stream with NS stages, K
 // walk rotated per workgroup, and (block decode form) pair lists built in the
 // kernel
@@ -199,13 +203,23 @@ struct DmaCfg {
 // a wave whose instruction finds its queue full stops issuing; when every
 // wave loads, both waves of a SIMD stall together and its MFMA pipe idles.
 // With producer waves, the other wave of each SIMD keeps issuing MFMAs.
+// Residual epilogue of the plain (non gate/up) form: the output becomes
+// scale * (acc + sum of `planes` bf16 planes of the output's shape).
+struct GemmResid {
+  const bf16* x = nullptr;
+  long long plane = 0;  // elements between planes
+  int planes = 0;
+  float scale = 1.f;
+};
+
 template <int BM, int BN, int WM, int WN, bool GATEUP, int BK, int NST, int PW, int GM,
-          bool PERSIST>
+          bool PERSIST, bool RESID = false>
 __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv,
                       int a_rows, const int32_t* __restrict__ offsets, int E, int rows,
                       const bf16* __restrict__ B0, const bf16* __restrict__ B1, int N, int K,
-                      bf16* __restrict__ out, int n_tiles_n, int n_tiles) {
+                      bf16* __restrict__ out, int n_tiles_n, int n_tiles, GemmResid res) {
+  static_assert(!(RESID && GATEUP), "residual epilogue on the plain form only");
   using C = DmaCfg<BM, BN, WM, WN, GATEUP, BK, NST, PW>;
   constexpr int NLD = C::NLD;
   __shared__ __align__(1024) unsigned char smem[NST * C::STAGE];
@@ -421,6 +435,34 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
       k_loop(std::false_type{});
 
     // epilogue: lane holds row m = .. + lane%32, columns n = .. + 8q + 4*(lane/32) + [0,4)
+    if constexpr (RESID) {
+      // residual planes added to the accumulators plane by plane, with the
+      // loads of all of the lane's outputs of one plane in flight together
+      for (int p = 0; p < res.planes; ++p) {
+        const bf16* xp = res.x + p * res.plane;
+        bf16x4 xv[C::SM][C::SN][4];
+#pragma unroll
+        for (int i = 0; i < C::SM; ++i)
+#pragma unroll
+          for (int j = 0; j < C::SN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int m = row0 + wm * C::WTM + i * 32 + lrow;
+              const int n = n0 + wn * C::WTN + j * 32 + q * 8 + (lane >> 5) * 4;
+              xv[i][j][q] = (m < row_end && n < N)
+                                ? *reinterpret_cast<const bf16x4*>(xp + (size_t)m * N + n)
+                                : bf16x4{};
+            }
+#pragma unroll
+        for (int i = 0; i < C::SM; ++i)
+#pragma unroll
+          for (int j = 0; j < C::SN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+              for (int v = 0; v < 4; ++v) acc[0][i][j][q * 4 + v] += (float)xv[i][j][q][v];
+      }
+    }
 #pragma unroll
     for (int i = 0; i < C::SM; ++i) {
       const int m = row0 + wm * C::WTM + i * 32 + lrow;
@@ -431,13 +473,19 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
         for (int q = 0; q < 4; ++q) {
           const int n = n0 + wn * C::WTN + j * 32 + q * 8 + (lane >> 5) * 4;
           if (n >= N) continue;
-          bf16x4 o;
+          float val[4];
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            float val = acc[0][i][j][q * 4 + v];
-            if constexpr (GATEUP) val = silu_f(val) * acc[C::NB - 1][i][j][q * 4 + v];
-            o[v] = (bf16)val;
+            val[v] = acc[0][i][j][q * 4 + v];
+            if constexpr (GATEUP) val[v] = silu_f(val[v]) * acc[C::NB - 1][i][j][q * 4 + v];
           }
+          if constexpr (RESID) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) val[v] *= res.scale;
+          }
+          bf16x4 o;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) o[v] = (bf16)val[v];
           *reinterpret_cast<bf16x4*>(out + (size_t)m * N + n) = o;
         }
       }
@@ -882,10 +930,12 @@ int device_cus() {
   return n / 8 * 8;
 }
 
-template <int BM, int BN, int WM, int WN, int BK, int NST, int PW, int GM, int PERSIST, bool GATEUP>
+template <int BM, int BN, int WM, int WN, int BK, int NST, int PW, int GM, int PERSIST, bool GATEUP,
+          bool RESID = false>
 void launch_gemm_dma(const bf16* A, const int32_t* gather, int kdiv, int a_rows,
                      const int32_t* offsets, int E, int rows, const bf16* B0, const bf16* B1,
-                     int N, int K, bf16* out, hipStream_t s, const char* name) {
+                     int N, int K, bf16* out, hipStream_t s, const char* name,
+                     GemmResid res = GemmResid{}) {
   const int ntn = ceil_div(N, BN);
   const int max_mt = ceil_div(rows, BM) + E;  // sum_e ceil(M_e/BM) <= rows/BM + E
   const long long n_tiles = (long long)max_mt * ntn;
@@ -896,16 +946,16 @@ void launch_gemm_dma(const bf16* A, const int32_t* gather, int kdiv, int a_rows,
   }
   dim3 grid((unsigned)nb);
   ProfileScope ps(name, s);
-  FOE_LAUNCH((grouped_gemm_dma<BM, BN, WM, WN, GATEUP, BK, NST, PW, GM, PERSIST != 0>), grid,
-                     dim3(WM * WN * kWave), 0, s, A, gather, kdiv, a_rows, offsets, E, rows, B0,
-                     B1, N, K, out, ntn, (int)n_tiles);
+  FOE_LAUNCH((grouped_gemm_dma<BM, BN, WM, WN, GATEUP, BK, NST, PW, GM, PERSIST != 0, RESID>),
+             grid, dim3(WM * WN * kWave), 0, s, A, gather, kdiv, a_rows, offsets, E, rows, B0, B1,
+             N, K, out, ntn, (int)n_tiles, res);
 }
 
 template <int BM, int BN, int WM, int WN, int BK, int NST, int PW, int GM, int PERSIST>
 struct DmaLaunch {
-  template <bool GATEUP, typename... Args>
+  template <bool GATEUP, bool RESID = false, typename... Args>
   static void run(Args... args) {
-    launch_gemm_dma<BM, BN, WM, WN, BK, NST, PW, GM, PERSIST, GATEUP>(args...);
+    launch_gemm_dma<BM, BN, WM, WN, BK, NST, PW, GM, PERSIST, GATEUP, RESID>(args...);
   }
 };
 
@@ -1011,6 +1061,22 @@ hipError_t launch_grouped_gemm(const void* A, const int32_t* offsets, int E, int
   DmaLaunch<FOE_DMA_DN>::run<false>(static_cast<const bf16*>(A), (const int32_t*)nullptr, 1, rows,
                                     offsets, E, rows, static_cast<const bf16*>(W),
                                     (const bf16*)nullptr, N, K, static_cast<bf16*>(out), s, name);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_resid(const void* A, const int32_t* offsets, int rows, const void* W,
+                             int N, int K, const void* x, int planes, long long plane,
+                             float scale, void* out, hipStream_t s, const char* name) {
+  if (rows == 0) return hipSuccess;
+  GemmResid res;
+  res.x = static_cast<const bf16*>(x);
+  res.plane = plane;
+  res.planes = planes;
+  res.scale = scale;
+  DmaLaunch<FOE_DMA_RES>::run<false, true>(static_cast<const bf16*>(A), (const int32_t*)nullptr,
+                                           1, rows, offsets, 1, rows, static_cast<const bf16*>(W),
+                                           (const bf16*)nullptr, N, K, static_cast<bf16*>(out), s,
+                                           name, res);
   return hipGetLastError();
 }
 

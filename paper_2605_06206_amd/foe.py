@@ -261,11 +261,12 @@ def cluster_block(x, w_router, bias, w_gate, w_up, w_down, k, reduce_scale=None,
 
 
 def group_attention(x, w_qkv, w_o, nq, theta, scale=1.0, out=None, ws=None, stream=None):
-    """foe_group_attention: x [H,S,d], w_qkv [H,(nq+2)*hd,d], w_o [H,d,nq*hd]
-    (bf16, hd = 128) -> r_full [S,d]."""
+    """foe_group_attention: x [H,S,d], w_qkv [H,(nq+2)*hd,d], w_o [d,H*nq*hd]
+    (the groups' output projections side by side; bf16, hd = 128) ->
+    r_full [S,d]."""
     H, S, d = x.shape
     hd = w_qkv.shape[1] // (nq + 2)
-    if tuple(w_qkv.shape) != (H, (nq + 2) * hd, d) or tuple(w_o.shape) != (H, d, nq * hd):
+    if tuple(w_qkv.shape) != (H, (nq + 2) * hd, d) or tuple(w_o.shape) != (d, H * nq * hd):
         raise FoeError(FOE_ERR_INVALID, f"group_attention: w_qkv {tuple(w_qkv.shape)} / w_o "
                        f"{tuple(w_o.shape)} do not match x {tuple(x.shape)} with nq={nq}")
     if out is None:

@@ -28,7 +28,7 @@ def _run(inp):
     c = inp["cfg"]
     x = to_dev(inp["x"])
     w_qkv = to_dev(np.stack([g["w_qkv"] for g in inp["groups"]]))
-    w_o = to_dev(np.stack([g["w_o"] for g in inp["groups"]]))
+    w_o = to_dev(np.concatenate([g["w_o"] for g in inp["groups"]], axis=1))
     out = foe.group_attention(x, w_qkv, w_o, c["nq"], c["theta"], c["scale"])
     torch.cuda.synchronize()
     return out.float().cpu().numpy()
@@ -50,6 +50,8 @@ def _check(inp, got):
     (3, 65, 64, 1, 10000.0, 1.0),       # odd query-head count, one key past a block
     (2, 130, 136, 4, 500000.0, 16.0),   # four query heads per key head, d off the tiles
     (1, 512, 128, 2, 500000.0, 1.0),    # eight key blocks, long-range rotary angles
+    (1, 64, 64, 2, 500000.0, 16.0),     # one full block: the second key half stays empty
+    (2, 320, 64, 2, 500000.0, 16.0),    # five key blocks: odd walks end on an empty step
 ])
 def test_group_attention_parity(H, S, d, nq, theta, scale):
     say("parity", H, S, d, nq, theta, scale)
@@ -87,6 +89,6 @@ def test_group_attention_deterministic_and_empty():
     assert np.array_equal(a, b)
     e = foe.group_attention(torch.empty((2, 0, 64), dtype=torch.bfloat16, device=DEV),
                             torch.empty((2, 512, 64), dtype=torch.bfloat16, device=DEV),
-                            torch.empty((2, 64, 256), dtype=torch.bfloat16, device=DEV), 2,
+                            torch.empty((64, 512), dtype=torch.bfloat16, device=DEV), 2,
                             500000.0)
     assert e.shape == (0, 64)
