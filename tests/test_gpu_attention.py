@@ -92,3 +92,51 @@ def test_group_attention_deterministic_and_empty():
                             torch.empty((64, 512), dtype=torch.bfloat16, device=DEV), 2,
                             500000.0)
     assert e.shape == (0, 64)
+
+
+def test_group_attention_graph_replay():
+    """The call captured in a HIP graph and replayed several times, with eager
+    work between the replays, gives the eager result every time."""
+    inp = synth.make_attention_inputs("attn_tiny_bf16")
+    c = inp["cfg"]
+    x = to_dev(inp["x"])
+    w_qkv = to_dev(np.stack([g["w_qkv"] for g in inp["groups"]]))
+    w_o = to_dev(np.concatenate([g["w_o"] for g in inp["groups"]], axis=1))
+    out = torch.empty((c["S"], c["d"]), dtype=torch.bfloat16, device=DEV)
+    n = foe.lib().foe_group_attention_workspace_bytes(c["H"], c["S"], c["d"], c["nq"], c["hd"])
+    ws = torch.empty(n, dtype=torch.uint8, device=DEV)
+    foe.group_attention(x, w_qkv, w_o, c["nq"], c["theta"], c["scale"], out=out, ws=ws)
+    torch.cuda.synchronize()
+    ref = out.clone()
+    side = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        foe.group_attention(x, w_qkv, w_o, c["nq"], c["theta"], c["scale"], out=out, ws=ws,
+                            stream=side)
+    say("graph replay")
+    for rep in range(3):
+        out.zero_()
+        ws.fill_(0xFF)  # the workspace holds no state between calls
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), rep
+
+
+def test_group_attention_long_sequence_sampled():
+    """S = 32768 (the paper's longest sequence) for one group: sampled query
+    rows against the per-row oracle (large key offsets, 512 key blocks)."""
+    cfg = dict(H=1, S=32768, d=512, nq=2, hd=128, theta=500000.0, scale=16.0, sigma=0.05,
+               seed=11)
+    inp = synth.make_attention_inputs(cfg)
+    say("long sequence", cfg)
+    got = _run(inp)
+    rows = [0, 1, 4095, 16384, 32766, 32767]
+    x = inp["x"].astype(np.float64)
+    g0 = inp["groups"][0]
+    ref = x[0, rows] + ao.group_attention_rows(x[0], g0["w_qkv"], g0["w_o"], cfg["nq"], cfg["hd"],
+                                               cfg["theta"], cfg["scale"], rows)
+    e_full = rel_err(got[rows], ref)
+    e_attn = rel_err(got[rows] - x[0, rows], ref - x[0, rows])
+    say(f"rel err r_full {e_full:.2e}, attention part {e_attn:.2e}")
+    assert e_full <= TOL and e_attn <= TOL
