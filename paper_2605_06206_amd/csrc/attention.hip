@@ -38,53 +38,80 @@ __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16*
                                                    int S, int s_pad, int nq, double theta,
                                                    double scale) {
   __shared__ double inv_freq[kHd / 2];
-  __shared__ __align__(16) bf16 vtile[kHd][kKB + 8];  // 144-byte rows
+  // V^T tile [128 dims][64 keys], 128-byte rows; 16-byte chunk cc of row dim
+  // in slot cc ^ ((dim >> 3) & 7), so that the 2-byte writes of the 16 lanes
+  // holding one key spread over 8 chunks
+  __shared__ __align__(16) bf16 vtile[kHd * kKB];
   const int tid = threadIdx.x;
   const int blk = blockIdx.x, grp = blockIdx.y;
   const size_t ld = (size_t)(nq + 2) * kHd;
   bf16* base = qkv + (size_t)grp * S * ld;
   if (tid < kHd / 2) inv_freq[tid] = pow(theta, -2.0 * tid / kHd);
-  __syncthreads();
 
-  const int i = tid & 63;
-  const double f = inv_freq[i];
-  constexpr double kTwoPi = 6.283185307179586476925286766559;
-  for (int j = 0; j < kQB / 4; ++j) {
-    const int s = blk * kQB + (tid >> 6) + 4 * j;
-    if (s >= S) break;
-    double a = (double)s / scale * f;
-    a -= kTwoPi * floor(a / kTwoPi);
-    float sn, cs;
-    sincosf((float)a, &sn, &cs);
-    bf16* row = base + (size_t)s * ld;
-    for (int h = 0; h <= nq; ++h) {
-      bf16* v = row + (size_t)h * kHd;
-      const float x1 = (float)v[i], x2 = (float)v[i + kHd / 2];
-      v[i] = (bf16)(x1 * cs - x2 * sn);
-      v[i + kHd / 2] = (bf16)(x2 * cs + x1 * sn);
-    }
-  }
-
+  // the value rows of the block: piece p = tid + 256 m is key p/16, dims
+  // 8 (p%16) .. +8 (loads go out before the rotation work)
+  bf16x8 vv[4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
     const int p = tid + 256 * m;
-    const int kl = p >> 4, c = p & 15;
-    const int s = blk * kKB + kl;
-    const bf16x8 v = s < S ? *reinterpret_cast<const bf16x8*>(base + (size_t)s * ld +
-                                                              (size_t)(nq + 1) * kHd + c * 8)
-                           : bf16x8{};
-    const int pk = vt_perm(kl);
+    const int s = blk * kKB + (p >> 4);
+    vv[m] = s < S ? *reinterpret_cast<const bf16x8*>(base + (size_t)s * ld +
+                                                     (size_t)(nq + 1) * kHd + (p & 15) * 8)
+                  : bf16x8{};
+  }
+  __syncthreads();
+
+  // rotary embedding: thread (row rs, pairs 4u .. 4u+3) for rows rs + 16 j;
+  // 8-byte accesses, a wave covers 4 rows per instruction
+  const int u = tid & 15, rs = tid >> 4;
+  constexpr double kTwoPi = 6.283185307179586476925286766559;
+  for (int j = 0; j < kQB / 16; ++j) {
+    const int s = blk * kQB + rs + 16 * j;
+    if (s >= S) break;
+    float cs[4], sn[4];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) vtile[c * 8 + e][pk] = v[e];
+    for (int e = 0; e < 4; ++e) {
+      double a = (double)s / scale * inv_freq[4 * u + e];
+      a -= kTwoPi * floor(a / kTwoPi);
+      sincosf((float)a, &sn[e], &cs[e]);
+    }
+    bf16* row = base + (size_t)s * ld + 4 * u;
+    for (int h = 0; h <= nq; ++h) {
+      bf16x4* lo = reinterpret_cast<bf16x4*>(row + (size_t)h * kHd);
+      bf16x4* hi = reinterpret_cast<bf16x4*>(row + (size_t)h * kHd + kHd / 2);
+      const bf16x4 x1 = *lo, x2 = *hi;
+      bf16x4 y1, y2;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float a1 = (float)x1[e], a2 = (float)x2[e];
+        y1[e] = (bf16)(a1 * cs[e] - a2 * sn[e]);
+        y2[e] = (bf16)(a2 * cs[e] + a1 * sn[e]);
+      }
+      *lo = y1;
+      *hi = y2;
+    }
+  }
+
+  // V^T through LDS
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const int p = tid + 256 * m;
+    const int c = p & 15;
+    const int pk = vt_perm(p >> 4);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int dim = c * 8 + e;
+      vtile[dim * kKB + (((pk >> 3) ^ ((dim >> 3) & 7)) << 3) + (pk & 7)] = vv[m][e];
+    }
   }
   __syncthreads();
   bf16* dst = vt + (size_t)grp * kHd * s_pad + (size_t)blk * kKB;
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
     const int p = tid + 256 * m;
-    const int dim = p >> 3, c = p & 7;
-    *reinterpret_cast<bf16x8*>(dst + (size_t)dim * s_pad + c * 8) =
-        *reinterpret_cast<const bf16x8*>(&vtile[dim][c * 8]);
+    const int dim = p >> 3, cc = p & 7;
+    *reinterpret_cast<bf16x8*>(dst + (size_t)dim * s_pad + cc * 8) =
+        *reinterpret_cast<const bf16x8*>(&vtile[dim * kKB + ((cc ^ ((dim >> 3) & 7)) << 3)]);
   }
 }
 
