@@ -73,7 +73,7 @@ KERNEL_SOURCES = {"route": "route.hip", "permute_index": "permute.hip",
                   "ffn_gateup": "ffn.hip", "ffn_down": "ffn.hip", "ffn_gateup_f32": "ffn.hip",
                   "ffn_down_f32": "ffn.hip", "combine": "combine.hip", "reduce": "combine.hip",
                   "attn_qkv": "ffn.hip", "attn_out": "ffn.hip", "attn_prep": "attention.hip",
-                  "attn_core": "attention.hip"}
+                  "attn_core": "attention.hip", "attn_xsum": "attention.hip"}
 
 
 def source_sha(kernel):
@@ -156,11 +156,14 @@ def attention_work(name, cfg):
         # and v are not algorithmic)
         return (4.0 * hd * nq * H * S * (S + 1) / 2,
                 2.0 * (rows * n_qkv + rows * nq * hd))
+    if name == "attn_xsum":
+        # the H residual planes read once, their fp32 sum written once
+        return 0.0, 2.0 * rows * d + 4.0 * S * d
     if name == "attn_out":
         # one product over the concatenated head outputs plus the residual
-        # planes: o, w_o and x read once, r_full written once
+        # sum: o, w_o and the fp32 sum read once, r_full written once
         return (2.0 * rows * nq * hd * d,
-                2.0 * (rows * nq * hd + H * d * nq * hd + rows * d + S * d))
+                2.0 * (rows * nq * hd + H * d * nq * hd + S * d) + 4.0 * S * d)
     return 0.0, 0.0
 
 

@@ -11,6 +11,8 @@
 // output projection of all groups as one GEMM over K = H*nq*hd whose epilogue
 // adds sum_h x[h] and scales by 1/H, so the per-group outputs never reach
 // memory.  The kernels below describe their layouts.
+#include <mutex>
+
 #include "foe_common.hpp"
 #include "lds_dma.hpp"
 
@@ -405,13 +407,70 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
 }
 
+// ---- residual sum -------------------------------------------------------------
+// xs = sum_h x[h] in fp32, h = 0..H-1 in order; 8 elements per thread and
+// grid-stride step.  It runs on a side stream beside the attention (which
+// reads little from HBM), so the output projection's epilogue reads one fp32
+// plane instead of H bf16 planes.
+__global__ __launch_bounds__(256) void xsum_kernel(const bf16* __restrict__ x, int H,
+                                                   long long plane, float* __restrict__ xs) {
+  const long long nvec = plane / 8;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < nvec;
+       i += (long long)gridDim.x * blockDim.x) {
+    float acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+#pragma unroll 4
+    for (int h = 0; h < H; ++h) {
+      const bf16x8 v = *reinterpret_cast<const bf16x8*>(x + (size_t)h * plane + i * 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += (float)v[e];
+    }
+    *reinterpret_cast<f32x4*>(xs + i * 8) = f32x4{acc[0], acc[1], acc[2], acc[3]};
+    *reinterpret_cast<f32x4*>(xs + i * 8 + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
+  }
+}
+
+// The side stream of the current device and the two events that fork it
+// from the caller's stream and join it back (created on first use, default
+// priority, kept until the process ends).  The fork / launch / join sequence
+// runs under one lock, so concurrent calls cannot interleave their event
+// records; under HIP-graph capture the fork and join become graph edges.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_side_mu;
+
+SideStream* side_stream_locked() {
+  static SideStream sides[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  SideStream& sd = sides[dev];
+  if (sd.s == nullptr) {
+    hipStream_t st = nullptr;
+    hipEvent_t f = nullptr, j = nullptr;
+    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&f, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&j, hipEventDisableTiming) != hipSuccess) {
+      if (f != nullptr) (void)hipEventDestroy(f);
+      (void)hipStreamDestroy(st);
+      return nullptr;
+    }
+    sd.s = st;
+    sd.fork = f;
+    sd.join = j;
+  }
+  return &sd;
+}
+
 __global__ void iota_kernel(int32_t* p, int n, int step) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = i * step;
 }
 
 struct AttnWs {
-  size_t offsets, qkv, vt, o, total;
+  size_t offsets, qkv, vt, o, xs, total;
 };
 
 AttnWs attn_ws(int H, int S, int d, int nq, int hd) {
@@ -427,6 +486,7 @@ AttnWs attn_ws(int H, int S, int d, int nq, int hd) {
   take(w.qkv, rows * (nq + 2) * hd * 2);
   take(w.vt, (size_t)H * hd * ceil_div(S, kKB) * kKB * 2);
   take(w.o, rows * nq * hd * 2);
+  take(w.xs, (size_t)S * d * 4);
   w.total = align_up(off, 256);
   return w;
 }
@@ -462,6 +522,26 @@ hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float the
     FOE_LAUNCH(prep_kernel, dim3(nqb, H), dim3(256), 0, s, qkv, vt, S, s_pad, nq, (double)theta,
                (double)scale);
   }
+  // the residual sum on the side stream, beside the attention
+  float* xs = reinterpret_cast<float*>(base + L.xs);
+  const long long plane = (long long)S * d;
+  std::unique_lock<std::mutex> lock(g_side_mu);
+  SideStream* side = side_stream_locked();
+  hipStream_t rs = s;
+  if (side != nullptr && hipEventRecord(side->fork, s) == hipSuccess &&
+      hipStreamWaitEvent(side->s, side->fork, 0) == hipSuccess)
+    rs = side->s;
+  {
+    ProfileScope ps("attn_xsum", rs);
+    const long long want = ceil_div(plane / 8, 256LL);
+#ifndef FOE_XSUM_WG
+#define FOE_XSUM_WG 256
+#endif
+    FOE_LAUNCH(xsum_kernel, dim3((unsigned)(want < FOE_XSUM_WG ? want : FOE_XSUM_WG)), dim3(256), 0,
+               rs,
+               static_cast<const bf16*>(x), H, plane, xs);
+  }
+  const bool joined = rs == s || (hipEventRecord(side->join, rs) == hipSuccess);
   {
     ProfileScope ps("attn_core", s);
     const float c_log2 = 1.4426950408889634f / sqrtf((float)hd);
@@ -472,11 +552,14 @@ hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float the
       FOE_LAUNCH(attn_fwd_kernel<1>, dim3(nqb * nq * H), dim3(256), 0, s, qkv, vt, S, s_pad, nq,
                  H, c_log2, o);
   }
+  if (!joined) return hipErrorUnknown;
+  if (rs != s && (e = hipStreamWaitEvent(s, side->join, 0)) != hipSuccess) return e;
+  lock.unlock();
   // output projection of all groups at once (o is [S][H*nq*hd], w_o
   // [d][H*nq*hd]) with the residual average in its epilogue:
-  // r_full = (o w_o^T + sum_h x[h]) / H; offsets[0..1] = {0, S}
-  e = launch_gemm_resid(o, offsets, S, w_o, d, H * nq * hd, x, H, (long long)S * d, 1.0f / H,
-                        r_full, s, "attn_out");
+  // r_full = (o w_o^T + xs) / H; offsets[0..1] = {0, S}
+  e = launch_gemm_resid(o, offsets, S, w_o, d, H * nq * hd, xs, 1.0f / H, r_full, s,
+                        "attn_out");
   if (e != hipSuccess) return e;
   return hipGetLastError();
 }

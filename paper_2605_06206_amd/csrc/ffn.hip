@@ -204,11 +204,9 @@ struct DmaCfg {
 // wave loads, both waves of a SIMD stall together and its MFMA pipe idles.
 // With producer waves, the other wave of each SIMD keeps issuing MFMAs.
 // Residual epilogue of the plain (non gate/up) form: the output becomes
-// scale * (acc + sum of `planes` bf16 planes of the output's shape).
+// scale * (acc + x), x an fp32 matrix of the output's shape.
 struct GemmResid {
-  const bf16* x = nullptr;
-  long long plane = 0;  // elements between planes
-  int planes = 0;
+  const float* x = nullptr;
   float scale = 1.f;
 };
 
@@ -436,32 +434,29 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
 
     // epilogue: lane holds row m = .. + lane%32, columns n = .. + 8q + 4*(lane/32) + [0,4)
     if constexpr (RESID) {
-      // residual planes added to the accumulators plane by plane, with the
-      // loads of all of the lane's outputs of one plane in flight together
-      for (int p = 0; p < res.planes; ++p) {
-        const bf16* xp = res.x + p * res.plane;
-        bf16x4 xv[C::SM][C::SN][4];
+      // the residual added to the accumulators, the loads of all of the
+      // lane's outputs in flight together
+      f32x4 xv[C::SM][C::SN][4];
 #pragma unroll
-        for (int i = 0; i < C::SM; ++i)
+      for (int i = 0; i < C::SM; ++i)
 #pragma unroll
-          for (int j = 0; j < C::SN; ++j)
+        for (int j = 0; j < C::SN; ++j)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int m = row0 + wm * C::WTM + i * 32 + lrow;
-              const int n = n0 + wn * C::WTN + j * 32 + q * 8 + (lane >> 5) * 4;
-              xv[i][j][q] = (m < row_end && n < N)
-                                ? *reinterpret_cast<const bf16x4*>(xp + (size_t)m * N + n)
-                                : bf16x4{};
-            }
+          for (int q = 0; q < 4; ++q) {
+            const int m = row0 + wm * C::WTM + i * 32 + lrow;
+            const int n = n0 + wn * C::WTN + j * 32 + q * 8 + (lane >> 5) * 4;
+            xv[i][j][q] = (m < row_end && n < N)
+                              ? *reinterpret_cast<const f32x4*>(res.x + (size_t)m * N + n)
+                              : f32x4{0.f, 0.f, 0.f, 0.f};
+          }
 #pragma unroll
-        for (int i = 0; i < C::SM; ++i)
+      for (int i = 0; i < C::SM; ++i)
 #pragma unroll
-          for (int j = 0; j < C::SN; ++j)
+        for (int j = 0; j < C::SN; ++j)
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
+          for (int q = 0; q < 4; ++q)
 #pragma unroll
-              for (int v = 0; v < 4; ++v) acc[0][i][j][q * 4 + v] += (float)xv[i][j][q][v];
-      }
+            for (int v = 0; v < 4; ++v) acc[0][i][j][q * 4 + v] += xv[i][j][q][v];
     }
 #pragma unroll
     for (int i = 0; i < C::SM; ++i) {
@@ -1065,13 +1060,11 @@ hipError_t launch_grouped_gemm(const void* A, const int32_t* offsets, int E, int
 }
 
 hipError_t launch_gemm_resid(const void* A, const int32_t* offsets, int rows, const void* W,
-                             int N, int K, const void* x, int planes, long long plane,
-                             float scale, void* out, hipStream_t s, const char* name) {
+                             int N, int K, const float* x, float scale, void* out, hipStream_t s,
+                             const char* name) {
   if (rows == 0) return hipSuccess;
   GemmResid res;
-  res.x = static_cast<const bf16*>(x);
-  res.plane = plane;
-  res.planes = planes;
+  res.x = x;
   res.scale = scale;
   DmaLaunch<FOE_DMA_RES>::run<false, true>(static_cast<const bf16*>(A), (const int32_t*)nullptr,
                                            1, rows, offsets, 1, rows, static_cast<const bf16*>(W),

@@ -123,11 +123,11 @@ hipError_t launch_expert_ffn(foe_dtype dt, int E, int d, int F, int rows, const 
 hipError_t launch_grouped_gemm(const void* A, const int32_t* offsets, int E, int rows,
                                const void* W, int N, int K, void* out, hipStream_t s,
                                const char* name);
-// out[m][n] = scale * (sum_k A[m][k] W[n][k] + sum_{p < planes} x[p*plane + m*N + n])
-// (bf16 in and out, fp32 sums; one segment of `rows` rows, offsets = {0, rows})
+// out[m][n] = scale * (sum_k A[m][k] W[n][k] + x[m*N + n]) (A, W, out bf16; x
+// fp32; fp32 sums; one segment of `rows` rows, offsets = {0, rows})
 hipError_t launch_gemm_resid(const void* A, const int32_t* offsets, int rows, const void* W,
-                             int N, int K, const void* x, int planes, long long plane,
-                             float scale, void* out, hipStream_t s, const char* name);
+                             int N, int K, const float* x, float scale, void* out, hipStream_t s,
+                             const char* name);
 // per-group attention of Table 3 (attention.hip): r_full [S, d] from x [H, S, d]
 size_t group_attention_scratch_bytes(int H, int S, int d, int nq, int hd);
 hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float theta, float scale,
