@@ -236,7 +236,7 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
  *   r_full[i] = (1/H) sum_h r[h,i]
  * computed as (1/H) (sum_h o[h,i] w_o[h]^T + sum_h x[h,i]) in fp32: the output
  * projections of all groups form one product over the concatenated head
- * outputs, and the residuals are added after it (h = 0..H-1 in order).
+ * outputs, and the residual sum (h = 0..H-1 in order) is added after it.
  * Attn_h: causal self-attention over the S tokens (positions 0..S-1) with one
  * key/value head and nq query heads sharing it (grouped-query attention),
  * scores q.k/sqrt(hd), rotary embedding on q and k pairing dimension i with
@@ -250,7 +250,11 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
  *   r_full   [S,d]            bf16 out
  *   ws, ws_bytes              workspace of foe_group_attention_workspace_bytes()
  * All pointers are device memory owned by the caller, 16-byte aligned (the
- * workspace too); the call enqueues work on `stream` and returns.  bf16 only
+ * workspace too); the call enqueues work on `stream` and returns.  One of its
+ * kernels (the residual sum) runs on a library-owned stream of the current
+ * device, forked from `stream` and joined back to it by events, so all of the
+ * call's work still follows earlier work on `stream` and precedes later work
+ * (also under HIP-graph capture, where the fork and join become edges).  bf16 only
  * and hd = 128 (else FOE_ERR_UNSUPPORTED); H*S*d and H*S*(nq+2)*hd must stay
  * below 2^30 elements.  S = 0 is a no-op.
  */
