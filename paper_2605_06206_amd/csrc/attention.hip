@@ -7,10 +7,11 @@
 //   r_full[i]  = (1/H) sum_h r[h, i]
 // Launches: the q/k/v projection of every group (one grouped GEMM with a
 // segment per group), a preparation pass (rotary embedding of q and k in
-// place, value head transposed), the attention (o as [S][H*nq*hd]), and the
-// output projection of all groups as one GEMM over K = H*nq*hd whose epilogue
-// adds sum_h x[h] and scales by 1/H, so the per-group outputs never reach
-// memory.  The kernels below describe their layouts.
+// place, value head transposed), the attention (o as [S][H*nq*hd]) with the
+// residual sum sum_h x[h] beside it on a side stream, and the output
+// projection of all groups as one GEMM over K = H*nq*hd whose epilogue adds
+// that sum and scales by 1/H, so the per-group outputs never reach memory.
+// The kernels below describe their layouts.
 #include <mutex>
 
 #include "foe_common.hpp"
@@ -25,9 +26,10 @@ constexpr int kKB = 64;   // keys per block
 
 // ---- preparation pass ----------------------------------------------------------
 // One workgroup per (64-row block, group).  (1) Rotary embedding of the q and
-// k heads in place: thread (row, i) forms the angle (s / scale) *
-// theta^(-2i/128) once, in double, reduced modulo 2*pi, and rotates the pair
-// (i, i + 64) of every q head and of the k head.  (2) The value head
+// k heads in place: each angle (s / scale) * theta^(-2i/128) is formed once,
+// in double, reduced modulo 2*pi, and rotates the pair (i, i + 64) of every q
+// head and of the k head (a thread takes 4 consecutive pairs of a row, 8-byte
+// accesses).  (2) The value head
 // transposed to vt[group][dim][key] (keys padded to s_pad with zeros), with
 // the keys of each 16-key group stored in the order 0-3, 8-11, 4-7, 12-15
 // (bits 2 and 3 swapped): that is the key order of the probabilities a lane
