@@ -466,13 +466,8 @@ SideStream* side_stream_locked() {
   return &sd;
 }
 
-__global__ void iota_kernel(int32_t* p, int n, int step) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = i * step;
-}
-
 struct AttnWs {
-  size_t offsets, qkv, vt, o, xs, total;
+  size_t qkv, vt, o, xs, total;
 };
 
 AttnWs attn_ws(int H, int S, int d, int nq, int hd) {
@@ -484,7 +479,6 @@ AttnWs attn_ws(int H, int S, int d, int nq, int hd) {
     field = off;
     off += bytes;
   };
-  take(w.offsets, (size_t)(H + 1) * 4);
   take(w.qkv, rows * (nq + 2) * hd * 2);
   take(w.vt, (size_t)H * hd * ceil_div(S, kKB) * kKB * 2);
   take(w.o, rows * nq * hd * 2);
@@ -505,15 +499,11 @@ hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float the
   if (S == 0) return hipSuccess;
   const AttnWs L = attn_ws(H, S, d, nq, hd);
   unsigned char* base = static_cast<unsigned char*>(scratch);
-  int32_t* offsets = reinterpret_cast<int32_t*>(base + L.offsets);
   bf16* qkv = reinterpret_cast<bf16*>(base + L.qkv);
   bf16* o = reinterpret_cast<bf16*>(base + L.o);
   const int rows = H * S;
-  {
-    ProfileScope ps("attn_offsets", s);
-    FOE_LAUNCH(iota_kernel, dim3(ceil_div(H + 1, 256)), dim3(256), 0, s, offsets, H + 1, S);
-  }
-  hipError_t e = launch_grouped_gemm(x, offsets, H, rows, w_qkv, (nq + 2) * hd, d, qkv, s,
+  // one segment of S rows per group (equal segments: no offsets array)
+  hipError_t e = launch_grouped_gemm(x, nullptr, H, rows, w_qkv, (nq + 2) * hd, d, qkv, s,
                                      "attn_qkv");
   if (e != hipSuccess) return e;
   bf16* vt = reinterpret_cast<bf16*>(base + L.vt);
@@ -559,8 +549,8 @@ hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float the
   lock.unlock();
   // output projection of all groups at once (o is [S][H*nq*hd], w_o
   // [d][H*nq*hd]) with the residual average in its epilogue:
-  // r_full = (o w_o^T + xs) / H; offsets[0..1] = {0, S}
-  e = launch_gemm_resid(o, offsets, S, w_o, d, H * nq * hd, xs, 1.0f / H, r_full, s,
+  // r_full = (o w_o^T + xs) / H
+  e = launch_gemm_resid(o, nullptr, S, w_o, d, H * nq * hd, xs, 1.0f / H, r_full, s,
                         "attn_out");
   if (e != hipSuccess) return e;
   return hipGetLastError();

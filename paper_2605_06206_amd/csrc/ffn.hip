@@ -59,12 +59,19 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // Number of M-tiles of BM rows over all experts (segments clamped as in
 // find_tile); every lane of the wave gets the total.
+// Start of segment e: offsets[e] clamped to [0, rows], or e * (rows / E) when
+// offsets is null (E segments of equal length, rows a multiple of E).
+__device__ __forceinline__ int seg_start(const int32_t* __restrict__ offsets, int e, int E,
+                                         int rows) {
+  return offsets == nullptr ? e * (rows / E) : min(max(offsets[e], 0), rows);
+}
+
 __device__ int total_mtiles(const int32_t* __restrict__ offsets, int E, int rows, int BM) {
   const int lane = lane_id();
   int mine = 0;
   for (int e = lane; e < E; e += kWave) {
-    const int a = min(max(offsets[e], 0), rows);
-    const int b = min(max(offsets[e + 1], 0), rows);
+    const int a = seg_start(offsets, e, E, rows);
+    const int b = seg_start(offsets, e + 1, E, rows);
     mine += b > a ? (b - a + BM - 1) / BM : 0;
   }
 #pragma unroll
@@ -83,8 +90,8 @@ __device__ bool find_tile(const int32_t* __restrict__ offsets, int E, int rows, 
   const int per = (E + kWave - 1) / kWave;
   const int e_begin = min(lane * per, E), e_end = min(e_begin + per, E);
   auto seg = [&](int e, int& a, int& b) {
-    a = min(max(offsets[e], 0), rows);
-    b = min(max(offsets[e + 1], 0), rows);
+    a = seg_start(offsets, e, E, rows);
+    b = seg_start(offsets, e + 1, E, rows);
     if (b < a) b = a;
   };
   int mine = 0;

@@ -120,11 +120,12 @@ hipError_t launch_expert_ffn(foe_dtype dt, int E, int d, int F, int rows, const 
 // bf16 grouped GEMM out[r] = A[r] W[e]^T for the rows r of segment e
 // (offsets [E+1]); W [E, N, K], A [rows, K], out [rows, N] (the down-projection
 // kernel of the expert FFN)
+// (offsets == nullptr: E segments of rows / E rows each)
 hipError_t launch_grouped_gemm(const void* A, const int32_t* offsets, int E, int rows,
                                const void* W, int N, int K, void* out, hipStream_t s,
                                const char* name);
 // out[m][n] = scale * (sum_k A[m][k] W[n][k] + x[m*N + n]) (A, W, out bf16; x
-// fp32; fp32 sums; one segment of `rows` rows, offsets = {0, rows})
+// fp32; fp32 sums; one segment of `rows` rows: offsets = {0, rows} or null)
 hipError_t launch_gemm_resid(const void* A, const int32_t* offsets, int rows, const void* W,
                              int N, int K, const float* x, float scale, void* out, hipStream_t s,
                              const char* name);
