@@ -52,6 +52,7 @@ def _check(inp, got):
     (1, 512, 128, 2, 500000.0, 1.0),    # eight key blocks, long-range rotary angles
     (1, 64, 64, 2, 500000.0, 16.0),     # one full block: the second key half stays empty
     (2, 320, 64, 2, 500000.0, 16.0),    # five key blocks: odd walks end on an empty step
+    (2, 150, 72, 3, 500000.0, 16.0),    # three query heads per key head, d = 72 (ragged K / N)
 ])
 def test_group_attention_parity(H, S, d, nq, theta, scale):
     say("parity", H, S, d, nq, theta, scale)
