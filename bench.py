@@ -381,8 +381,8 @@ def main():
         copy_calibration()
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: the per-cluster block has no multi-GPU path in "
-              "this build (use --gpus 1)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
+              "(use --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

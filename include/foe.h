@@ -53,7 +53,7 @@ extern "C" {
 typedef enum {
     FOE_OK = 0,
     FOE_ERR_INVALID = -1,     /* bad shape, null/misaligned pointer, bad dtype */
-    FOE_ERR_UNSUPPORTED = -2, /* valid request this build does not implement */
+    FOE_ERR_UNSUPPORTED = -2, /* valid request the library does not implement */
     FOE_ERR_WORKSPACE = -3,   /* ws_bytes below foe_workspace_bytes()        */
     FOE_ERR_HIP = -4          /* the HIP runtime reported an error            */
 } foe_status;

@@ -14,7 +14,7 @@ What it computes (Table 3, FoE column, first two rows; Section 3.1):
 
 Each group owns one KV head (the paper ties the groups to the KV heads) and
 ``nq`` query heads that share it (grouped-query attention).  Readings where
-the paper is silent (each is listed in the design doc):
+the paper is silent:
 
 * ``Attn_h`` is causal self-attention over the S tokens of the sequence at
   positions 0..S-1, scores ``q.k / sqrt(hd)``, softmax over the keys up to and

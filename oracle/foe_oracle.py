@@ -16,7 +16,7 @@ What the block computes (one cluster, i.e. one expert group ``h`` of the paper):
   group partials are averaged, ``(1/H) sum_h``; Section 3.2 states that groups
   sharing one GPU combine their partials locally.
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent:
 
 * the router is a linear map ``W_r [E,d]`` with an optional bias ``[E]``;
 * selection is decided on fp32 scores, descending, equal scores -> lower id;
