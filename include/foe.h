@@ -255,7 +255,7 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
  * device, forked from `stream` and joined back to it by events, so all of the
  * call's work still follows earlier work on `stream` and precedes later work
  * (also under HIP-graph capture, where the fork and join become edges).  bf16 only
- * and hd = 128 (else FOE_ERR_UNSUPPORTED); H*S*d and H*S*(nq+2)*hd must stay
+ * and hd = 96 or 128 (else FOE_ERR_UNSUPPORTED); H*S*d and H*S*(nq+2)*hd must stay
  * below 2^30 elements.  S = 0 is a no-op.
  */
 int foe_group_attention(foe_dtype dt, int H, int S, int d, int nq, int hd, float theta,

@@ -20,7 +20,9 @@
 namespace foe {
 namespace {
 
-constexpr int kHd = 128;  // head dimension the attention kernel is built for
+// head dimensions the kernels are built for: 128 (the 7B model) and 96 (the
+// 1B model); a K tile row is 256 bytes either way (dims past hd read zeros)
+constexpr int kHdMax = 128;
 constexpr int kQB = 64;   // queries per workgroup and head
 constexpr int kKB = 64;   // keys per block
 
@@ -38,38 +40,42 @@ __device__ __forceinline__ int vt_perm(int key) {
   return (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
 }
 
+template <int HD>
 __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16* __restrict__ vt,
                                                    int S, int s_pad, int nq, double theta,
                                                    double scale) {
-  __shared__ double inv_freq[kHd / 2];
-  // V^T tile [128 dims][64 keys], 128-byte rows; 16-byte chunk cc of row dim
+  constexpr int CPR = HD / 8;  // 16-byte chunks of a head row
+  constexpr int PPT = CPR / 4; // value pieces per thread (64 keys x CPR chunks)
+  __shared__ double inv_freq[HD / 2];
+  // V^T tile [HD dims][64 keys], 128-byte rows; 16-byte chunk cc of row dim
   // in slot cc ^ ((dim >> 3) & 7), so that the 2-byte writes of the 16 lanes
   // holding one key spread over 8 chunks
-  __shared__ __align__(16) bf16 vtile[kHd * kKB];
+  __shared__ __align__(16) bf16 vtile[HD * kKB];
   const int tid = threadIdx.x;
   const int blk = blockIdx.x, grp = blockIdx.y;
-  const size_t ld = (size_t)(nq + 2) * kHd;
+  const size_t ld = (size_t)(nq + 2) * HD;
   bf16* base = qkv + (size_t)grp * S * ld;
-  if (tid < kHd / 2) inv_freq[tid] = pow(theta, -2.0 * tid / kHd);
+  if (tid < HD / 2) inv_freq[tid] = pow(theta, -2.0 * tid / HD);
 
-  // the value rows of the block: piece p = tid + 256 m is key p/16, dims
-  // 8 (p%16) .. +8 (loads go out before the rotation work)
-  bf16x8 vv[4];
+  // the value rows of the block: piece p = tid + 256 m is key p / CPR, dims
+  // 8 (p % CPR) .. +8 (loads go out before the rotation work)
+  bf16x8 vv[PPT];
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
+  for (int m = 0; m < PPT; ++m) {
     const int p = tid + 256 * m;
-    const int s = blk * kKB + (p >> 4);
+    const int s = blk * kKB + p / CPR;
     vv[m] = s < S ? *reinterpret_cast<const bf16x8*>(base + (size_t)s * ld +
-                                                     (size_t)(nq + 1) * kHd + (p & 15) * 8)
+                                                     (size_t)(nq + 1) * HD + (p % CPR) * 8)
                   : bf16x8{};
   }
   __syncthreads();
 
   // rotary embedding: thread (row rs, pairs 4u .. 4u+3) for rows rs + 16 j;
-  // 8-byte accesses, a wave covers 4 rows per instruction
+  // 8-byte accesses, a wave covers 4 rows per instruction (threads with
+  // 4u >= HD/2 have no pairs)
   const int u = tid & 15, rs = tid >> 4;
   constexpr double kTwoPi = 6.283185307179586476925286766559;
-  for (int j = 0; j < kQB / 16; ++j) {
+  for (int j = 0; j < kQB / 16 && 4 * u < HD / 2; ++j) {
     const int s = blk * kQB + rs + 16 * j;
     if (s >= S) break;
     float cs[4], sn[4];
@@ -81,8 +87,8 @@ __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16*
     }
     bf16* row = base + (size_t)s * ld + 4 * u;
     for (int h = 0; h <= nq; ++h) {
-      bf16x4* lo = reinterpret_cast<bf16x4*>(row + (size_t)h * kHd);
-      bf16x4* hi = reinterpret_cast<bf16x4*>(row + (size_t)h * kHd + kHd / 2);
+      bf16x4* lo = reinterpret_cast<bf16x4*>(row + (size_t)h * HD);
+      bf16x4* hi = reinterpret_cast<bf16x4*>(row + (size_t)h * HD + HD / 2);
       const bf16x4 x1 = *lo, x2 = *hi;
       bf16x4 y1, y2;
 #pragma unroll
@@ -98,10 +104,10 @@ __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16*
 
   // V^T through LDS
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
+  for (int m = 0; m < PPT; ++m) {
     const int p = tid + 256 * m;
-    const int c = p & 15;
-    const int pk = vt_perm(p >> 4);
+    const int c = p % CPR;
+    const int pk = vt_perm(p / CPR);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int dim = c * 8 + e;
@@ -109,9 +115,9 @@ __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16*
     }
   }
   __syncthreads();
-  bf16* dst = vt + (size_t)grp * kHd * s_pad + (size_t)blk * kKB;
+  bf16* dst = vt + (size_t)grp * HD * s_pad + (size_t)blk * kKB;
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
+  for (int m = 0; m < HD / 32; ++m) {  // HD rows x 8 chunks
     const int p = tid + 256 * m;
     const int dim = p >> 3, cc = p & 7;
     *reinterpret_cast<bf16x8*>(dst + (size_t)dim * s_pad + cc * 8) =
@@ -149,17 +155,21 @@ __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16*
 // log2), so probabilities stay below 2^8 and the accumulators are rescaled
 // only on those (wave-uniform) steps; the final O / l cancels m exactly.
 // Masking (causal, and keys past S) runs only on the blocks that need it.
-template <int NH>
+template <int NH, int HD>
 __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(
     const bf16* __restrict__ qkv, const bf16* __restrict__ vt, int S, int s_pad, int nq, int H,
     float c_log2, bf16* __restrict__ out) {
   constexpr int HW = 2 * NH;            // waves per half
-  constexpr int KT = kKB * kHd * 2;     // K tile bytes
-  constexpr int VT = kHd * kKB * 2;     // V^T tile bytes
+  constexpr int KT = kKB * kHdMax * 2;  // K tile bytes (256-byte rows)
+  constexpr int VT = HD * kKB * 2;      // V^T tile bytes
+  constexpr int NST = HD / 16;          // score k-steps (16 dims each)
+  constexpr int NDT = HD / 32;          // output tiles (32 dims each)
   constexpr int HALF = 2 * KT + 2 * VT; // LDS bytes per half
   constexpr int KI = KT / 1024 / HW;    // DMA instructions per wave and tile
   constexpr int VI = VT / 1024 / HW;
-  static_assert(HW * 64 * 64 * 4 <= 2 * HALF, "merge buffer fits in the rings");
+  static_assert(HD == 96 || HD == 128, "head dimension");
+  static_assert(VT % (1024 * HW) == 0, "V^T DMA splits evenly over the waves");
+  static_assert(HW * 64 * (HD / 2 + 2) * 4 <= 2 * HALF, "merge buffer fits in the rings");
   __shared__ __align__(1024) unsigned char smem[2 * HALF];
 
   const int tid = threadIdx.x;
@@ -177,18 +187,18 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int rest = r % P;
   const int grp = rest / hgs;
   const int head = (rest % hgs) * NH + (hw >> 1);
-  const size_t ld = (size_t)(nq + 2) * kHd;
+  const size_t ld = (size_t)(nq + 2) * HD;
   const bf16* gbase = qkv + (size_t)grp * S * ld;
   const int q0 = qb * kQB + (hw & 1) * 32;  // this wave's first query
   const int qi = lane & 31, hl = lane >> 5;
   const int q = q0 + qi;
 
   // Q^T fragments: query q, dims 16 st + 8 hl + [0, 8)
-  bf16x8 qf[8];
+  bf16x8 qf[NST];
   {
-    const bf16* qrow = gbase + (size_t)min(q, S - 1) * ld + (size_t)head * kHd + hl * 8;
+    const bf16* qrow = gbase + (size_t)min(q, S - 1) * ld + (size_t)head * HD + hl * 8;
 #pragma unroll
-    for (int st = 0; st < 8; ++st) {
+    for (int st = 0; st < NST; ++st) {
       qf[st] = *reinterpret_cast<const bf16x8*>(qrow + st * 16);
       if (q >= S) qf[st] = bf16x8{};
     }
@@ -197,21 +207,23 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
   // otherwise wait for them (vmcnt(0)) inside the loop, which also waits for
   // the LDS-DMA of the next block issued there.
 #pragma unroll
-  for (int st = 0; st < 8; ++st) asm volatile("" ::"v"(qf[st]));
+  for (int st = 0; st < NST; ++st) asm volatile("" ::"v"(qf[st]));
 
   // DMA: K instruction g = hw*KI + i fills key rows 4g .. 4g+3 (lane ->
   // row 4g + lane/16, slot lane%16); V^T instruction g fills dim rows 8g ..
   // 8g+7 (lane -> row 8g + lane/8, slot lane%8).  Keys past S read zeros
   // (the K range ends at the group's last row; V^T is zero-padded).
   const __amdgpu_buffer_rsrc_t rk =
-      make_rsrc_u(gbase + (size_t)nq * kHd, (uint32_t)(((size_t)S * ld - (size_t)nq * kHd) * 2));
+      make_rsrc_u(gbase + (size_t)nq * HD, (uint32_t)(((size_t)S * ld - (size_t)nq * HD) * 2));
   const __amdgpu_buffer_rsrc_t rv =
-      make_rsrc_u(vt + (size_t)grp * kHd * s_pad, (uint32_t)((size_t)kHd * s_pad * 2));
+      make_rsrc_u(vt + (size_t)grp * HD * s_pad, (uint32_t)((size_t)HD * s_pad * 2));
   uint32_t koff[KI], voff[VI];
 #pragma unroll
   for (int i = 0; i < KI; ++i) {
     const int row = 4 * (hw * KI + i) + (lane >> 4);
-    koff[i] = (uint32_t)((size_t)row * ld * 2) + (uint32_t)((((lane & 15) ^ (row & 15))) << 4);
+    const int chunk = (lane & 15) ^ (row & 15);
+    // chunks past the head (HD < 128) read zeros and are never used
+    koff[i] = chunk < HD / 8 ? (uint32_t)((size_t)row * ld * 2) + (uint32_t)(chunk << 4) : kOob;
   }
 #pragma unroll
   for (int i = 0; i < VI; ++i) {
@@ -236,7 +248,7 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
   };
   auto pv = [&](f32x16* oacc, const bf16x8* pf, const unsigned char* vs) {
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
+    for (int dt = 0; dt < NDT; ++dt) {
       const int row = dt * 32 + qi;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -247,9 +259,9 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
   };
 
-  f32x16 oacc[4];
+  f32x16 oacc[NDT];
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int t = 0; t < NDT; ++t)
 #pragma unroll
     for (int v = 0; v < 16; ++v) oacc[t][v] = 0.f;
   float m_run = -__builtin_inff();  // running maximum of query q, scaled (log2 units)
@@ -288,7 +300,7 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
         for (int v = 0; v < 16; ++v) sacc[t][v] = 0.f;
 #pragma unroll
-      for (int st = 0; st < 8; ++st)
+      for (int st = 0; st < NST; ++st)
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           const int row = t * 32 + qi;
@@ -299,7 +311,7 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
     if (resc) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
+      for (int t = 0; t < NDT; ++t)
 #pragma unroll
         for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
     }
@@ -360,7 +372,7 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
   vm_barrier<0>();
   if (resc) {
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+    for (int t = 0; t < NDT; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
   }
@@ -370,25 +382,25 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
   // (the rings are free after this barrier)
   float l = l_run + __shfl_xor(l_run, 32);
   __syncthreads();
-  float* mb = reinterpret_cast<float*>(smem) + (size_t)hw * (64 * 66);
+  float* mb = reinterpret_cast<float*>(smem) + (size_t)hw * (64 * (HD / 2 + 2));
   if (half == 1) {
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+    for (int t = 0; t < NDT; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) mb[(t * 16 + v) * 64 + lane] = oacc[t][v];
-    mb[64 * 64 + lane] = m_run;
-    mb[65 * 64 + lane] = l;
+    mb[(HD / 2) * 64 + lane] = m_run;
+    mb[(HD / 2 + 1) * 64 + lane] = l;
   }
   __syncthreads();
   if (half == 1) return;
   {
-    const float mo = mb[64 * 64 + lane], lo = mb[65 * 64 + lane];
+    const float mo = mb[(HD / 2) * 64 + lane], lo = mb[(HD / 2 + 1) * 64 + lane];
     const float m = fmaxf(m_run, mo);
     const float a0 = m_run == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(m_run - m);
     const float a1 = mo == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(mo - m);
     l = l * a0 + lo * a1;
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+    for (int t = 0; t < NDT; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) oacc[t][v] = oacc[t][v] * a0 + mb[(t * 16 + v) * 64 + lane] * a1;
   }
@@ -396,9 +408,9 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
   // O[q][dim] = O^T / l; lane holds dims 32 dt + 8 g + 4 hl + [0, 4)
   if (q < S) {
     const float inv = 1.f / l;
-    bf16* orow = out + ((size_t)q * H + grp) * ((size_t)nq * kHd) + (size_t)head * kHd;
+    bf16* orow = out + ((size_t)q * H + grp) * ((size_t)nq * HD) + (size_t)head * HD;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
+    for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         bf16x4 o;
@@ -511,8 +523,12 @@ hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float the
   const int s_pad = nqb * kKB;
   {
     ProfileScope ps("attn_prep", s);
-    FOE_LAUNCH(prep_kernel, dim3(nqb, H), dim3(256), 0, s, qkv, vt, S, s_pad, nq, (double)theta,
-               (double)scale);
+    if (hd == 96)
+      FOE_LAUNCH(prep_kernel<96>, dim3(nqb, H), dim3(256), 0, s, qkv, vt, S, s_pad, nq,
+                 (double)theta, (double)scale);
+    else
+      FOE_LAUNCH(prep_kernel<128>, dim3(nqb, H), dim3(256), 0, s, qkv, vt, S, s_pad, nq,
+                 (double)theta, (double)scale);
   }
   // the residual sum on the side stream, beside the attention
   float* xs = reinterpret_cast<float*>(base + L.xs);
@@ -537,12 +553,22 @@ hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float the
   {
     ProfileScope ps("attn_core", s);
     const float c_log2 = 1.4426950408889634f / sqrtf((float)hd);
-    if (nq % 2 == 0)
-      FOE_LAUNCH(attn_fwd_kernel<2>, dim3(nqb * (nq / 2) * H), dim3(512), 0, s, qkv, vt, S, s_pad,
-                 nq, H, c_log2, o);
-    else
-      FOE_LAUNCH(attn_fwd_kernel<1>, dim3(nqb * nq * H), dim3(256), 0, s, qkv, vt, S, s_pad, nq,
-                 H, c_log2, o);
+    const dim3 g2(nqb * (nq / 2) * H), g1(nqb * nq * H);
+    if (hd == 96) {
+      if (nq % 2 == 0)
+        FOE_LAUNCH((attn_fwd_kernel<2, 96>), g2, dim3(512), 0, s, qkv, vt, S, s_pad, nq, H,
+                   c_log2, o);
+      else
+        FOE_LAUNCH((attn_fwd_kernel<1, 96>), g1, dim3(256), 0, s, qkv, vt, S, s_pad, nq, H,
+                   c_log2, o);
+    } else {
+      if (nq % 2 == 0)
+        FOE_LAUNCH((attn_fwd_kernel<2, 128>), g2, dim3(512), 0, s, qkv, vt, S, s_pad, nq, H,
+                   c_log2, o);
+      else
+        FOE_LAUNCH((attn_fwd_kernel<1, 128>), g1, dim3(256), 0, s, qkv, vt, S, s_pad, nq, H,
+                   c_log2, o);
+    }
   }
   if (!joined) return hipErrorUnknown;
   if (rs != s && (e = hipStreamWaitEvent(s, side->join, 0)) != hipSuccess) return e;

@@ -438,7 +438,7 @@ size_t foe_group_attention_workspace_bytes(int H, int S, int d, int nq, int hd) 
   c.need(S >= 0, "S must be >= 0");
   check_dim8(c, d, "d must be a positive multiple of 8");
   c.need(nq >= 1 && nq <= 64, "nq must be in [1, 64]");
-  c.need(hd == 128, "hd must be 128");
+  c.need(hd == 96 || hd == 128, "hd must be 96 or 128");
   if (!c.err.empty()) return (g_err = c.err, SIZE_MAX);
   return group_attention_scratch_bytes(H, S, d, nq, hd);
 }
@@ -459,8 +459,8 @@ int foe_group_attention(foe_dtype dt, int H, int S, int d, int nq, int hd, float
   c.tensor(w_o, any, "w_o");
   c.tensor(r_full, any, "r_full");
   if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_group_attention: " + c.err);
-  if (dt != FOE_BF16 || hd != 128)
-    return fail(FOE_ERR_UNSUPPORTED, "foe_group_attention: bf16 with hd = 128 only");
+  if (dt != FOE_BF16 || (hd != 96 && hd != 128))
+    return fail(FOE_ERR_UNSUPPORTED, "foe_group_attention: bf16 with hd = 96 or 128 only");
   const long long rows = (long long)H * S;
   if (!(operand_fits(rows, d, 2) && operand_fits(rows, (long long)(nq + 2) * hd, 2)))
     return fail(FOE_ERR_UNSUPPORTED,

@@ -262,7 +262,7 @@ def cluster_block(x, w_router, bias, w_gate, w_up, w_down, k, reduce_scale=None,
 
 def group_attention(x, w_qkv, w_o, nq, theta, scale=1.0, out=None, ws=None, stream=None):
     """foe_group_attention: x [H,S,d], w_qkv [H,(nq+2)*hd,d], w_o [d,H*nq*hd]
-    (the groups' output projections side by side; bf16, hd = 128) ->
+    (the groups' output projections side by side; bf16, hd = 96 or 128) ->
     r_full [S,d]."""
     H, S, d = x.shape
     hd = w_qkv.shape[1] // (nq + 2)

@@ -126,6 +126,8 @@ ATTN_CONFIGS = {
                            sigma=0.05, seed=6),
     "attn_share_bf16": dict(H=8, S=4096, d=2048, nq=2, hd=128, theta=500000.0, scale=16.0,
                             sigma=0.02, seed=5),
+    "attn_small_bf16": dict(H=8, S=4096, d=768, nq=1, hd=96, theta=500000.0, scale=16.0,
+                            sigma=0.035, seed=7),
 }
 
 

@@ -113,11 +113,12 @@ def test_group_attention_rejects(L):
     n = L.foe_group_attention_workspace_bytes(8, 4096, 2048, 2, 128)
     assert 0 < n < SIZE_MAX
     assert L.foe_group_attention_workspace_bytes(8, 4096, 2048, 2, 64) == SIZE_MAX
-    assert "hd must be 128" in foe.last_error()
+    assert "hd must be 96 or 128" in foe.last_error()
+    assert 0 < L.foe_group_attention_workspace_bytes(8, 4096, 2048, 1, 96) < SIZE_MAX
     f = ctypes.c_float
     ok = [BF16, 2, 64, 64, 2, 128, f(500000.0), f(16.0), P, P, P, P]
     bad = list(ok)
-    bad[5] = 96
+    bad[5] = 64
     assert L.foe_group_attention(*bad, P2, n, None) == foe.FOE_ERR_UNSUPPORTED
     bad = list(ok)
     bad[0] = F32

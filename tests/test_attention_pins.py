@@ -6,6 +6,7 @@ routine), closed forms for one token and for equal keys, causality under
 perturbation of later tokens, and the cross-group average of identical groups.
 """
 import numpy as np
+import pytest
 import torch
 
 from oracle import attention_oracle as ao
@@ -23,9 +24,10 @@ def _rope_complex(v, S, hd, theta, scale):
     return np.concatenate([w.real, w.imag], axis=1)
 
 
-def test_rope_matches_complex_rotation_and_keeps_norms():
+@pytest.mark.parametrize("hd", [96, 128])
+def test_rope_matches_complex_rotation_and_keeps_norms(hd):
     rng = np.random.default_rng(1)
-    S, hd = 37, 128
+    S = 37
     v = rng.standard_normal((S, hd))
     for theta, scale in ((10000.0, 1.0), (500000.0, 16.0)):
         cos, sin = ao.rope_angles(S, hd, theta, scale)
@@ -37,9 +39,10 @@ def test_rope_matches_complex_rotation_and_keeps_norms():
         assert np.max(np.abs(r[:, :h] ** 2 + r[:, h:] ** 2 - v[:, :h] ** 2 - v[:, h:] ** 2)) <= 1e-12
 
 
-def test_rope_scores_depend_on_relative_position_only():
+@pytest.mark.parametrize("hd", [96, 128])
+def test_rope_scores_depend_on_relative_position_only(hd):
     rng = np.random.default_rng(2)
-    S, hd = 40, 128
+    S = 40
     q0, k0 = rng.standard_normal(hd), rng.standard_normal(hd)
     cos, sin = ao.rope_angles(S, hd, 500000.0, 16.0)
     q = ao.apply_rope(np.tile(q0, (S, 1)), cos, sin)
@@ -56,11 +59,12 @@ def _qkv_parts(S=23, d=32, nq=2, hd=128, seed=3):
     return x, w_qkv, w_o
 
 
-def test_attention_matches_torch_sdpa():
+@pytest.mark.parametrize("nq,hd", [(3, 128), (1, 96)])
+def test_attention_matches_torch_sdpa(nq, hd):
     """The core softmax attention against torch's causal SDPA in fp64 on the
     oracle's own rotated q, k and v (the key/value head repeated for every
     query head: grouped-query attention)."""
-    S, d, nq, hd = 29, 32, 3, 128
+    S, d = 29, 32
     x, w_qkv, w_o = _qkv_parts(S, d, nq, hd, seed=4)
     out, parts = ao.group_attention(x, w_qkv, w_o, nq, hd, 500000.0, 16.0)
     q = torch.from_numpy(parts["q"]).permute(1, 0, 2)            # [nq, S, hd]

@@ -44,28 +44,35 @@ def _check(inp, got):
     assert e_full <= TOL and e_attn <= TOL
 
 
-@pytest.mark.parametrize("H,S,d,nq,theta,scale", [
-    (2, 200, 256, 2, 500000.0, 16.0),   # ragged last query / key block
-    (1, 1, 64, 2, 500000.0, 16.0),      # one token
-    (3, 65, 64, 1, 10000.0, 1.0),       # odd query-head count, one key past a block
-    (2, 130, 136, 4, 500000.0, 16.0),   # four query heads per key head, d off the tiles
-    (1, 512, 128, 2, 500000.0, 1.0),    # eight key blocks, long-range rotary angles
-    (1, 64, 64, 2, 500000.0, 16.0),     # one full block: the second key half stays empty
-    (2, 320, 64, 2, 500000.0, 16.0),    # five key blocks: odd walks end on an empty step
-    (2, 150, 72, 3, 500000.0, 16.0),    # three query heads per key head, d = 72 (ragged K / N)
+@pytest.mark.parametrize("H,S,d,nq,hd,theta,scale", [
+    (2, 200, 256, 2, 128, 500000.0, 16.0),   # ragged last query / key block
+    (1, 1, 64, 2, 128, 500000.0, 16.0),      # one token
+    (3, 65, 64, 1, 128, 10000.0, 1.0),       # odd query-head count, one key past a block
+    (2, 130, 136, 4, 128, 500000.0, 16.0),   # four query heads per key head, d off the tiles
+    (1, 512, 128, 2, 128, 500000.0, 1.0),    # eight key blocks, long-range rotary angles
+    (1, 64, 64, 2, 128, 500000.0, 16.0),     # one full block: the second key half stays empty
+    (2, 320, 64, 2, 128, 500000.0, 16.0),    # five key blocks: odd walks end on an empty step
+    (2, 150, 72, 3, 128, 500000.0, 16.0),    # three query heads per key head, d = 72
+    (2, 200, 96, 1, 96, 500000.0, 16.0),     # hd = 96 (the 1B model), one query head
+    (3, 330, 120, 2, 96, 500000.0, 16.0),    # hd = 96, two query heads, six key blocks
+    (1, 1, 64, 1, 96, 500000.0, 16.0),       # hd = 96, one token
+    (2, 129, 64, 3, 96, 10000.0, 1.0),       # hd = 96, odd head count, one key past 2 blocks
 ])
-def test_group_attention_parity(H, S, d, nq, theta, scale):
-    say("parity", H, S, d, nq, theta, scale)
-    cfg = dict(H=H, S=S, d=d, nq=nq, hd=128, theta=theta, scale=scale, sigma=0.05,
-               seed=H * 1000 + S)
+def test_group_attention_parity(H, S, d, nq, hd, theta, scale):
+    say("parity", H, S, d, nq, hd, theta, scale)
+    cfg = dict(H=H, S=S, d=d, nq=nq, hd=hd, theta=theta, scale=scale, sigma=0.05,
+               seed=H * 1000 + S + (hd if hd != 128 else 0))
     inp = synth.make_attention_inputs(cfg)
     _check(inp, _run(inp))
 
 
-def test_group_attention_full_size_sampled():
-    """The 8-group, 4096-token configuration: sampled query rows (first, block
-    edges, last) against the per-row oracle."""
-    inp = synth.make_attention_inputs("attn_share_bf16")
+@pytest.mark.parametrize("name", ["attn_share_bf16", "attn_small_bf16"])
+def test_group_attention_full_size_sampled(name):
+    """The 8-group, 4096-token configurations of the 7B (hd = 128, two query
+    heads per group) and 1B (hd = 96, d = 768, one query head per group)
+    models: sampled query rows (first, block edges, last) against the per-row
+    oracle."""
+    inp = synth.make_attention_inputs(name)
     c = inp["cfg"]
     say("full size", c)
     got = _run(inp)
