@@ -28,8 +28,8 @@ constexpr int kKB = 64;   // keys per block
 
 // ---- preparation pass ----------------------------------------------------------
 // One workgroup per (64-row block, group).  (1) Rotary embedding of the q and
-// k heads in place: each angle (s / scale) * theta^(-2i/128) is formed once,
-// in double, reduced modulo 2*pi, and rotates the pair (i, i + 64) of every q
+// k heads in place: each angle (s / scale) * theta^(-2i/HD) is formed once,
+// in double, reduced modulo 2*pi, and rotates the pair (i, i + HD/2) of every q
 // head and of the k head (a thread takes 4 consecutive pairs of a row, 8-byte
 // accesses).  (2) The value head
 // transposed to vt[group][dim][key] (keys padded to s_pad with zeros), with
@@ -138,8 +138,8 @@ __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16*
 // Each half streams its key blocks through its own 2-stage LDS rings filled by
 // LDS-DMA:
 //   K tile   [64 keys][128 dims], 256-byte rows, 16-byte chunk c in slot
-//            c ^ (key & 15);
-//   V^T tile [128 dims][64 keys], 128-byte rows, chunk c in slot c ^ swz8(dim).
+//            c ^ (key & 15) (at HD = 96 the chunks past the head hold zeros);
+//   V^T tile [HD dims][64 keys], 128-byte rows, chunk c in slot c ^ swz8(dim).
 // Scores come out transposed, S^T = K Q^T (v_mfma_f32_32x32x16_bf16, A = K
 // rows, B = Q^T held in registers): lane l holds 32 scores of query l%32, at
 // keys 32t + 8(v/4) + 4(l/32) + v%4 of tile t.  Its 8 scores of key step u

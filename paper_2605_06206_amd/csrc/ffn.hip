@@ -31,9 +31,18 @@
 #ifndef FOE_DMA_DN
 #define FOE_DMA_DN 256, 256, 2, 4, 64, 2, 4, 4, 1
 #endif
-// plain GEMM with the residual epilogue (few M rows: 128 x 256 tiles)
+// plain grouped GEMM over a few wide segments (the q/k/v projection of the
+// attention groups): as the down projection, tiles walked XCD by XCD
+#ifndef FOE_DMA_SEG
+#define FOE_DMA_SEG 256, 256, 2, 4, 64, 2, 4, 4, 2
+#endif
+// plain GEMM with the residual epilogue (few M rows: 128 x 256 tiles, or
+// 128 x 128 when the larger tiles would leave compute units idle)
 #ifndef FOE_DMA_RES
 #define FOE_DMA_RES 128, 256, 2, 4, 64, 2, 3, 4, 1
+#endif
+#ifndef FOE_DMA_RES_SMALL
+#define FOE_DMA_RES_SMALL 128, 128, 2, 4, 64, 2, 4, 4, 1
 #endif
 // few rows per expert (decode): LDS-staged weight stream with NS stages, K
 // walk rotated per workgroup, and (block decode form) pair lists built in the
@@ -218,7 +227,7 @@ struct GemmResid {
 };
 
 template <int BM, int BN, int WM, int WN, bool GATEUP, int BK, int NST, int PW, int GM,
-          bool PERSIST, bool RESID = false>
+          int PERSIST, bool RESID = false>
 __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv,
                       int a_rows, const int32_t* __restrict__ offsets, int E, int rows,
@@ -512,20 +521,32 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
       nt = i / g;
     }
   };
-  if constexpr (PERSIST) {
+  auto run_t = [&](int t) {
+    int mt, nt, e, row0, row_end;
+    tile_coords(t, mt, nt);
+    if (!find_tile(offsets, E, rows, BM, mt, e, row0, row_end)) return;
+    vm_barrier<0>();  // the previous tile's LDS reads are done everywhere
+    run_tile(e, row0, row_end, nt);
+  };
+  if constexpr (PERSIST == 2) {
+    // one workgroup per CU, each XCD walks a contiguous eighth of the tile
+    // order (workgroup b runs on XCD b % 8; the grid is a multiple of 8), so
+    // the N-tiles of an M-tile and the M-tiles of a segment meet in that
+    // XCD's own L2: for a few wide segments (one per XCD) every A row and
+    // weight slice is fetched from memory once
+    const int n_real = m_tiles * n_tiles_n;
+    const int x = blockIdx.x % 8, per = gridDim.x / 8;
+    const int chunk = (n_real + 7) / 8;
+    const int t_end = min((x + 1) * chunk, n_real);
+    for (int t = x * chunk + (int)blockIdx.x / 8; t < t_end; t += per) run_t(t);
+  } else if constexpr (PERSIST == 1) {
     // one workgroup per CU, tiles dealt round-robin: the tiles running at any
     // moment are a window of consecutive tiles of the order above, spread
     // over all XCDs, and their shared A rows and weight slices meet in the
     // Infinity Cache that every XCD reads through (measured faster than
-    // giving each XCD a contiguous range for its own L2)
+    // giving each XCD a contiguous range for its own L2 on the expert GEMMs)
     const int n_real = m_tiles * n_tiles_n;
-    for (int t = blockIdx.x; t < n_real; t += gridDim.x) {
-      int mt, nt, e, row0, row_end;
-      tile_coords(t, mt, nt);
-      if (!find_tile(offsets, E, rows, BM, mt, e, row0, row_end)) continue;
-      vm_barrier<0>();  // the previous tile's LDS reads are done everywhere
-      run_tile(e, row0, row_end, nt);
-    }
+    for (int t = blockIdx.x; t < n_real; t += gridDim.x) run_t(t);
   } else {
     const int tile = blockIdx.x;
     if (tile >= n_tiles) return;
@@ -948,7 +969,7 @@ void launch_gemm_dma(const bf16* A, const int32_t* gather, int kdiv, int a_rows,
   }
   dim3 grid((unsigned)nb);
   ProfileScope ps(name, s);
-  FOE_LAUNCH((grouped_gemm_dma<BM, BN, WM, WN, GATEUP, BK, NST, PW, GM, PERSIST != 0, RESID>),
+  FOE_LAUNCH((grouped_gemm_dma<BM, BN, WM, WN, GATEUP, BK, NST, PW, GM, PERSIST, RESID>),
              grid, dim3(WM * WN * kWave), 0, s, A, gather, kdiv, a_rows, offsets, E, rows, B0, B1,
              N, K, out, ntn, (int)n_tiles, res);
 }
@@ -1060,7 +1081,7 @@ hipError_t launch_grouped_gemm(const void* A, const int32_t* offsets, int E, int
                                const void* W, int N, int K, void* out, hipStream_t s,
                                const char* name) {
   if (rows == 0) return hipSuccess;
-  DmaLaunch<FOE_DMA_DN>::run<false>(static_cast<const bf16*>(A), (const int32_t*)nullptr, 1, rows,
+  DmaLaunch<FOE_DMA_SEG>::run<false>(static_cast<const bf16*>(A), (const int32_t*)nullptr, 1, rows,
                                     offsets, E, rows, static_cast<const bf16*>(W),
                                     (const bf16*)nullptr, N, K, static_cast<bf16*>(out), s, name);
   return hipGetLastError();
@@ -1073,10 +1094,17 @@ hipError_t launch_gemm_resid(const void* A, const int32_t* offsets, int rows, co
   GemmResid res;
   res.x = x;
   res.scale = scale;
-  DmaLaunch<FOE_DMA_RES>::run<false, true>(static_cast<const bf16*>(A), (const int32_t*)nullptr,
-                                           1, rows, offsets, 1, rows, static_cast<const bf16*>(W),
-                                           (const bf16*)nullptr, N, K, static_cast<bf16*>(out), s,
-                                           name, res);
+  static const int cus = device_cus();
+  if ((long long)ceil_div(rows, 128) * ceil_div(N, 256) < cus)
+    DmaLaunch<FOE_DMA_RES_SMALL>::run<false, true>(
+        static_cast<const bf16*>(A), (const int32_t*)nullptr, 1, rows, offsets, 1, rows,
+        static_cast<const bf16*>(W), (const bf16*)nullptr, N, K, static_cast<bf16*>(out), s, name,
+        res);
+  else
+    DmaLaunch<FOE_DMA_RES>::run<false, true>(
+        static_cast<const bf16*>(A), (const int32_t*)nullptr, 1, rows, offsets, 1, rows,
+        static_cast<const bf16*>(W), (const bf16*)nullptr, N, K, static_cast<bf16*>(out), s, name,
+        res);
   return hipGetLastError();
 }
 
