@@ -24,7 +24,9 @@ namespace {
 // 1B model); a K tile row is 256 bytes either way (dims past hd read zeros)
 constexpr int kHdMax = 128;
 constexpr int kQB = 64;   // queries per workgroup and head
-constexpr int kKB = 64;   // keys per block
+constexpr int kKB = 64;   // keys per block of the V^T layout (its zero padding)
+// floor of the running maximum (log2 units): finite, and far below any score
+constexpr float kMFloor = -1.0e30f;
 
 // ---- preparation pass ----------------------------------------------------------
 // One workgroup per (64-row block, group).  (1) Rotary embedding of the q and
@@ -127,19 +129,20 @@ __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16*
 
 // ---- attention ----------------------------------------------------------------
 // Task: 64 queries of NH query heads of one group (the heads share the
-// group's key/value head and so its LDS tiles).  A workgroup has two halves
-// of 2*NH waves; wave (half, head hh, query half qw) holds 32 queries.  The
-// halves split the task's key blocks of 64 (half 0 the even ones, half 1 the
-// odd ones) and merge their partial softmax states through LDS at the end, so
-// that every running workgroup keeps two waves on each SIMD however short its
-// task.  Tasks are numbered longest first; with one workgroup per compute unit
-// the dispatcher hands the next task to the first unit that frees up, which
-// balances the causal walks.
-// Each half streams its key blocks through its own 2-stage LDS rings filled by
-// LDS-DMA:
-//   K tile   [64 keys][128 dims], 256-byte rows, 16-byte chunk c in slot
+// group's key/value head and so its LDS tiles).  A workgroup of 8 waves has
+// NP parts of 2*NH waves; wave (part, head hh, query half qw) holds 32
+// queries.  The parts split the task's key blocks (part p takes blocks p,
+// p + NP, ...) and merge their partial softmax states through LDS at the end,
+// so that every running workgroup keeps two waves on each SIMD however short
+// its task: two heads per task use 2 parts of 64-key blocks, one head (nq
+// odd) 4 parts of 32-key blocks.  Tasks are numbered longest first; with one
+// workgroup per compute unit the dispatcher hands the next task to the first
+// unit that frees up, which balances the causal walks.
+// Each part streams its key blocks (KB keys) through its own 2-stage LDS
+// rings filled by LDS-DMA:
+//   K tile   [KB keys][128 dims], 256-byte rows, 16-byte chunk c in slot
 //            c ^ (key & 15) (at HD = 96 the chunks past the head hold zeros);
-//   V^T tile [HD dims][64 keys], 128-byte rows, chunk c in slot c ^ swz8(dim).
+//   V^T tile [HD dims][KB keys], 2 KB-byte rows, chunk c in slot c ^ swz(dim).
 // Scores come out transposed, S^T = K Q^T (v_mfma_f32_32x32x16_bf16, A = K
 // rows, B = Q^T held in registers): lane l holds 32 scores of query l%32, at
 // keys 32t + 8(v/4) + 4(l/32) + v%4 of tile t.  Its 8 scores of key step u
@@ -147,7 +150,7 @@ __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16*
 // reads the V^T tile in the same key order (the permuted layout written by
 // the preparation pass).
 // Software pipeline: an iteration computes the scores of its block, then the
-// P V product of the half's previous block while the softmax of the new block
+// P V product of the part's previous block while the softmax of the new block
 // runs on the vector ALUs (independent instructions, interleaved); the K ring
 // runs one block ahead, the V ring one block behind.
 // Online softmax in base 2 with a lazily updated maximum: the running maximum
@@ -155,30 +158,35 @@ __global__ __launch_bounds__(256) void prep_kernel(bf16* __restrict__ qkv, bf16*
 // log2), so probabilities stay below 2^8 and the accumulators are rescaled
 // only on those (wave-uniform) steps; the final O / l cancels m exactly.
 // Masking (causal, and keys past S) runs only on the blocks that need it.
-template <int NH, int HD>
-__global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(
+template <int NH, int HD, int NP>
+__global__ __launch_bounds__(NP * NH * 128) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(
     const bf16* __restrict__ qkv, const bf16* __restrict__ vt, int S, int s_pad, int nq, int H,
     float c_log2, bf16* __restrict__ out) {
-  constexpr int HW = 2 * NH;            // waves per half
-  constexpr int KT = kKB * kHdMax * 2;  // K tile bytes (256-byte rows)
-  constexpr int VT = HD * kKB * 2;      // V^T tile bytes
+  constexpr int KB = 128 / NP;          // keys per block (64 with 2 parts, 32 with 4)
+  constexpr int HW = 2 * NH;            // waves per part
+  constexpr int KT = KB * kHdMax * 2;   // K tile bytes (256-byte rows)
+  constexpr int VT = HD * KB * 2;       // V^T tile bytes (rows of 2 KB bytes)
+  constexpr int VC = KB / 8;            // 16-byte chunks of a V^T row
   constexpr int NST = HD / 16;          // score k-steps (16 dims each)
   constexpr int NDT = HD / 32;          // output tiles (32 dims each)
-  constexpr int HALF = 2 * KT + 2 * VT; // LDS bytes per half
+  constexpr int NSC = KB / 32;          // score tiles per block (32 keys each)
+  constexpr int NKS = KB / 16;          // P V key steps per block
+  constexpr int PART = 2 * KT + 2 * VT; // LDS bytes per part
   constexpr int KI = KT / 1024 / HW;    // DMA instructions per wave and tile
   constexpr int VI = VT / 1024 / HW;
   static_assert(HD == 96 || HD == 128, "head dimension");
-  static_assert(VT % (1024 * HW) == 0, "V^T DMA splits evenly over the waves");
-  static_assert(HW * 64 * (HD / 2 + 2) * 4 <= 2 * HALF, "merge buffer fits in the rings");
-  __shared__ __align__(1024) unsigned char smem[2 * HALF];
+  static_assert((NP == 2 || NP == 4) && NP * NH * 2 == 8, "8 waves: 2 parts x 2 heads or 4 x 1");
+  static_assert(KT % (1024 * HW) == 0 && VT % (1024 * HW) == 0, "DMA splits evenly over the waves");
+  static_assert((NP - 1) * HW * 64 * (HD / 2 + 2) * 4 <= NP * PART, "merge buffers fit in the rings");
+  __shared__ __align__(1024) unsigned char smem[NP * PART];
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid >> 6;
-  const int half = wave / HW;        // key blocks half, half + 2, ...
-  const int hw = wave % HW;          // wave within its half
+  const int part = wave / HW;        // key blocks part, part + NP, ...
+  const int hw = wave % HW;          // wave within its part
   const int hw_u = __builtin_amdgcn_readfirstlane(hw);
-  const int half_u = __builtin_amdgcn_readfirstlane(half);
+  const int part_u = __builtin_amdgcn_readfirstlane(part);
   const int nqb = (S + kQB - 1) / kQB;
   const int hgs = nq / NH;
   const int P = hgs * H;
@@ -210,8 +218,8 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
   for (int st = 0; st < NST; ++st) asm volatile("" ::"v"(qf[st]));
 
   // DMA: K instruction g = hw*KI + i fills key rows 4g .. 4g+3 (lane ->
-  // row 4g + lane/16, slot lane%16); V^T instruction g fills dim rows 8g ..
-  // 8g+7 (lane -> row 8g + lane/8, slot lane%8).  Keys past S read zeros
+  // row 4g + lane/16, slot lane%16); V^T instruction g fills the 64 / VC dim
+  // rows from g*64/VC (lane -> row g*64/VC + lane/VC, slot lane%VC).  Keys past S read zeros
   // (the K range ends at the group's last row; V^T is zero-padded).
   const __amdgpu_buffer_rsrc_t rk =
       make_rsrc_u(gbase + (size_t)nq * HD, (uint32_t)(((size_t)S * ld - (size_t)nq * HD) * 2));
@@ -227,22 +235,22 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
 #pragma unroll
   for (int i = 0; i < VI; ++i) {
-    const int row = 8 * (hw * VI + i) + (lane >> 3);
-    voff[i] = (uint32_t)row * s_pad * 2u + (uint32_t)(((lane & 7) ^ swz<8>(row)) << 4);
+    const int row = (64 / VC) * (hw * VI + i) + lane / VC;
+    voff[i] = (uint32_t)row * s_pad * 2u + (uint32_t)(((lane % VC) ^ swz<VC>(row)) << 4);
   }
-  unsigned char* hs = smem + half * HALF;  // this half's rings
-  const uint32_t hbase = lds_addr(smem) + (uint32_t)half_u * HALF;
-  // the half's i-th block (key block 2i + half) -> K stage i&1 (bytes
+  unsigned char* hs = smem + part * PART;  // this part's rings
+  const uint32_t hbase = lds_addr(smem) + (uint32_t)part_u * PART;
+  // the part's i-th block (key block NP i + part) -> K stage i&1 (bytes
   // [0, 2 KT)), V^T stage i&1 (bytes [2 KT, 2 KT + 2 VT))
   auto issue_k = [&](int i) {
-    const uint32_t kstep = (uint32_t)(2 * i + half) * kKB * (uint32_t)ld * 2u;
+    const uint32_t kstep = (uint32_t)(NP * i + part) * KB * (uint32_t)ld * 2u;
     const uint32_t lk = hbase + (uint32_t)(i & 1) * KT + (uint32_t)hw_u * KI * 1024;
 #pragma unroll
     for (int j = 0; j < KI; ++j) dma16(rk, koff[j] + kstep, lk, j * 1024);
   };
   auto issue_v = [&](int i) {
     const uint32_t lv = hbase + 2 * KT + (uint32_t)(i & 1) * VT + (uint32_t)hw_u * VI * 1024;
-    const uint32_t vstep = (uint32_t)(2 * i + half) * kKB * 2u;
+    const uint32_t vstep = (uint32_t)(NP * i + part) * KB * 2u;
 #pragma unroll
     for (int j = 0; j < VI; ++j) dma16(rv, voff[j] + vstep, lv, j * 1024);
   };
@@ -251,9 +259,9 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
     for (int dt = 0; dt < NDT; ++dt) {
       const int row = dt * 32 + qi;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const bf16x8 vf =
-            *reinterpret_cast<const bf16x8*>(vs + row * 128 + (((u * 2 + hl) ^ swz<8>(row)) << 4));
+      for (int u = 0; u < NKS; ++u) {
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vs + row * (KB * 2) +
+                                                           (((u * 2 + hl) ^ swz<VC>(row)) << 4));
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[u], oacc[dt], 0, 0, 0);
       }
     }
@@ -264,45 +272,48 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
   for (int t = 0; t < NDT; ++t)
 #pragma unroll
     for (int v = 0; v < 16; ++v) oacc[t][v] = 0.f;
-  float m_run = -__builtin_inff();  // running maximum of query q, scaled (log2 units)
+  // running maximum of query q, scaled (log2 units); it starts at a finite
+  // floor so that a row whose keys in a block are all masked (possible in a
+  // part's first block with 32-key blocks) gets p = 2^-inf = 0, not NaN
+  float m_run = kMFloor;
   float l_run = 0.f;                // this lane's share of the running sum
   float alpha = 1.f;                // rescale owed to oacc before the next P V
   bool resc = false;                // (wave-uniform) some lane owes a rescale
-  bf16x8 pf[4];                     // probabilities of the previous block (B operand)
+  bf16x8 pf[NKS];                   // probabilities of the previous block (B operand)
 #pragma unroll
-  for (int u = 0; u < 4; ++u) pf[u] = bf16x8{};
-  // P V steps with P = 0 (the first iteration, and the last one of a half
+  for (int u = 0; u < NKS; ++u) pf[u] = bf16x8{};
+  // P V steps with P = 0 (the first iteration, and the last one of a part
   // left without a block) may read a V stage no DMA has filled: zero both
-  // stages of both halves so that they add exact zeros
-  for (int i = tid; i < 4 * (VT / 16); i += NH * 256) {
+  // stages of every part so that they add exact zeros
+  for (int i = tid; i < NP * 2 * (VT / 16); i += NP * NH * 128) {
     const int h = i / (2 * (VT / 16)), c = i % (2 * (VT / 16));
-    *reinterpret_cast<u32x4*>(smem + h * HALF + 2 * KT + c * 16) = u32x4{0u, 0u, 0u, 0u};
+    *reinterpret_cast<u32x4*>(smem + h * PART + 2 * KT + c * 16) = u32x4{0u, 0u, 0u, 0u};
   }
 
-  const int nkb = min(qb + 1, (S + kKB - 1) / kKB);
-  const int niter = (nkb + 1) / 2;  // both halves run the same iterations
-  if (half < nkb) issue_k(0);
+  const int nkb = min((qb + 1) * (kQB / KB), (S + KB - 1) / KB);
+  const int niter = (nkb + NP - 1) / NP;  // every part runs the same iterations
+  if (part < nkb) issue_k(0);
   for (int it = 0; it < niter; ++it) {
-    const int kb = 2 * it + half;
+    const int kb = NP * it + part;
     const bool valid = kb < nkb;  // wave-uniform
     // K of this block and V of the previous one have landed for every wave,
     // and every wave is done with the previous iteration's stages
     vm_barrier<0>();
-    if (kb + 2 < nkb) issue_k(it + 1);
+    if (kb + NP < nkb) issue_k(it + 1);
     if (valid) issue_v(it);
     const unsigned char* ks = hs + (it & 1) * KT;
     const unsigned char* vs = hs + 2 * KT + ((it + 1) & 1) * VT;  // previous block's V
 
-    f32x16 sacc[2];
+    f32x16 sacc[NSC];
     if (valid) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < NSC; ++t)
 #pragma unroll
         for (int v = 0; v < 16; ++v) sacc[t][v] = 0.f;
 #pragma unroll
       for (int st = 0; st < NST; ++st)
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
+        for (int t = 0; t < NSC; ++t) {
           const int row = t * 32 + qi;
           const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
               ks + row * 256 + (((st * 2 + hl) ^ (row & 15)) << 4));
@@ -315,10 +326,10 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
         for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
     }
-    const int kbase = kb * kKB;
-    if (valid && (kbase + kKB - 1 > q0 || kbase + kKB > S)) {  // wave-uniform
+    const int kbase = kb * KB;
+    if (valid && (kbase + KB - 1 > q0 || kbase + KB > S)) {  // wave-uniform
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < NSC; ++t)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int key = kbase + t * 32 + (v >> 2) * 8 + hl * 4 + (v & 3);
@@ -333,14 +344,14 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
       // softmax of this block
       float mx = sacc[0][0];
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < NSC; ++t)
 #pragma unroll
         for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[t][v]);
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       const float mxs = mx * c_log2;
-      // every row sees a key in its half's first block (half 0: key 0; half
-      // 1, which has blocks only when qb >= 1: key 64, as q >= 64 and
-      // S > 64), so mxs is finite and that first block always moves m
+      // a row with a visible key in the block has a finite mxs, far above
+      // the floor, so the first such block always moves m; a row without one
+      // (mxs = -inf) keeps m and gets p = 0
       const bool need = mxs > m_run + 8.f;
       const float m_new = need ? mxs : m_run;
       alpha = need ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
@@ -348,7 +359,7 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
       resc = __builtin_amdgcn_ballot_w64(need) != 0;
       float ps = 0.f;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < NKS; ++u) {
         bf16x8 p8;
 #pragma unroll
         for (int e = 0; e < 8; ++e)
@@ -365,10 +376,10 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
       resc = false;
       alpha = 1.f;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) pf[u] = bf16x8{};
+      for (int u = 0; u < NKS; ++u) pf[u] = bf16x8{};
     }
   }
-  // the last block's P V (P = 0 if the half's last iteration had no block)
+  // the last block's P V (P = 0 if the part's last iteration had no block)
   vm_barrier<0>();
   if (resc) {
 #pragma unroll
@@ -378,12 +389,14 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
   pv(oacc, pf, hs + 2 * KT + ((niter + 1) & 1) * VT);
 
-  // merge: half 1 hands (m, l, O) to its partner wave of half 0 through LDS
-  // (the rings are free after this barrier)
+  // merge: parts 1 .. NP-1 hand (m, l, O) to their partner wave of part 0
+  // through LDS (the rings are free after this barrier); part 0 folds them
+  // in part order
   float l = l_run + __shfl_xor(l_run, 32);
   __syncthreads();
-  float* mb = reinterpret_cast<float*>(smem) + (size_t)hw * (64 * (HD / 2 + 2));
-  if (half == 1) {
+  constexpr int MB = 64 * (HD / 2 + 2);  // floats per wave buffer
+  if (part != 0) {
+    float* mb = reinterpret_cast<float*>(smem) + (size_t)((part - 1) * HW + hw) * MB;
 #pragma unroll
     for (int t = 0; t < NDT; ++t)
 #pragma unroll
@@ -392,17 +405,21 @@ __global__ __launch_bounds__(NH * 256) __attribute__((amdgpu_waves_per_eu(2, 2))
     mb[(HD / 2 + 1) * 64 + lane] = l;
   }
   __syncthreads();
-  if (half == 1) return;
-  {
+  if (part != 0) return;
+#pragma unroll
+  for (int pp = 1; pp < NP; ++pp) {
+    const float* mb = reinterpret_cast<const float*>(smem) + (size_t)((pp - 1) * HW + hw) * MB;
     const float mo = mb[(HD / 2) * 64 + lane], lo = mb[(HD / 2 + 1) * 64 + lane];
     const float m = fmaxf(m_run, mo);
-    const float a0 = m_run == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(m_run - m);
-    const float a1 = mo == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(mo - m);
+    // both maxima are at least the finite floor, so the factors are finite
+    const float a0 = __builtin_amdgcn_exp2f(m_run - m);
+    const float a1 = __builtin_amdgcn_exp2f(mo - m);
     l = l * a0 + lo * a1;
 #pragma unroll
     for (int t = 0; t < NDT; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) oacc[t][v] = oacc[t][v] * a0 + mb[(t * 16 + v) * 64 + lane] * a1;
+    m_run = m;
   }
 
   // O[q][dim] = O^T / l; lane holds dims 32 dt + 8 g + 4 hl + [0, 4)
@@ -553,20 +570,22 @@ hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float the
   {
     ProfileScope ps("attn_core", s);
     const float c_log2 = 1.4426950408889634f / sqrtf((float)hd);
+    // two heads per task: two parts of 64-key blocks; one head: four parts
+    // of 32-key blocks (8 waves either way)
     const dim3 g2(nqb * (nq / 2) * H), g1(nqb * nq * H);
     if (hd == 96) {
       if (nq % 2 == 0)
-        FOE_LAUNCH((attn_fwd_kernel<2, 96>), g2, dim3(512), 0, s, qkv, vt, S, s_pad, nq, H,
+        FOE_LAUNCH((attn_fwd_kernel<2, 96, 2>), g2, dim3(512), 0, s, qkv, vt, S, s_pad, nq, H,
                    c_log2, o);
       else
-        FOE_LAUNCH((attn_fwd_kernel<1, 96>), g1, dim3(256), 0, s, qkv, vt, S, s_pad, nq, H,
+        FOE_LAUNCH((attn_fwd_kernel<1, 96, 4>), g1, dim3(512), 0, s, qkv, vt, S, s_pad, nq, H,
                    c_log2, o);
     } else {
       if (nq % 2 == 0)
-        FOE_LAUNCH((attn_fwd_kernel<2, 128>), g2, dim3(512), 0, s, qkv, vt, S, s_pad, nq, H,
+        FOE_LAUNCH((attn_fwd_kernel<2, 128, 2>), g2, dim3(512), 0, s, qkv, vt, S, s_pad, nq, H,
                    c_log2, o);
       else
-        FOE_LAUNCH((attn_fwd_kernel<1, 128>), g1, dim3(256), 0, s, qkv, vt, S, s_pad, nq, H,
+        FOE_LAUNCH((attn_fwd_kernel<1, 128, 4>), g1, dim3(512), 0, s, qkv, vt, S, s_pad, nq, H,
                    c_log2, o);
     }
   }
