@@ -57,6 +57,8 @@ def _check(inp, got):
     (3, 330, 120, 2, 96, 500000.0, 16.0),    # hd = 96, two query heads, six key blocks
     (1, 1, 64, 1, 96, 500000.0, 16.0),       # hd = 96, one token
     (2, 129, 64, 3, 96, 10000.0, 1.0),       # hd = 96, odd head count, one key past 2 blocks
+    (1, 32, 64, 1, 96, 500000.0, 16.0),      # one head: exactly one 32-key block
+    (2, 97, 64, 1, 128, 500000.0, 16.0),     # one head, hd = 128: one key past three 32-key blocks
 ])
 def test_group_attention_parity(H, S, d, nq, hd, theta, scale):
     say("parity", H, S, d, nq, hd, theta, scale)
@@ -131,10 +133,12 @@ def test_group_attention_graph_replay():
         assert torch.equal(out, ref), rep
 
 
-def test_group_attention_long_sequence_sampled():
+@pytest.mark.parametrize("nq,hd", [(2, 128), (1, 96)])
+def test_group_attention_long_sequence_sampled(nq, hd):
     """S = 32768 (the paper's longest sequence) for one group: sampled query
-    rows against the per-row oracle (large key offsets, 512 key blocks)."""
-    cfg = dict(H=1, S=32768, d=512, nq=2, hd=128, theta=500000.0, scale=16.0, sigma=0.05,
+    rows against the per-row oracle (large key offsets, 512 blocks of 64 keys
+    with two heads per task, 1024 blocks of 32 with one)."""
+    cfg = dict(H=1, S=32768, d=512, nq=nq, hd=hd, theta=500000.0, scale=16.0, sigma=0.05,
                seed=11)
     inp = synth.make_attention_inputs(cfg)
     say("long sequence", cfg)
