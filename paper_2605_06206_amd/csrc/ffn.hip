@@ -37,12 +37,13 @@
 #define FOE_DMA_SEG 256, 256, 2, 4, 64, 2, 4, 4, 2
 #endif
 // plain GEMM with the residual epilogue (few M rows: 128 x 256 tiles, or
-// 128 x 128 when the larger tiles would leave compute units idle)
+// 128 x 128 when the larger tiles would leave compute units idle); one tile
+// per CU walks all of K, so a third LDS stage keeps more loads in flight
 #ifndef FOE_DMA_RES
-#define FOE_DMA_RES 128, 256, 2, 4, 64, 2, 3, 4, 1
+#define FOE_DMA_RES 128, 256, 2, 4, 64, 3, 3, 4, 1
 #endif
 #ifndef FOE_DMA_RES_SMALL
-#define FOE_DMA_RES_SMALL 128, 128, 2, 4, 64, 2, 4, 4, 1
+#define FOE_DMA_RES_SMALL 128, 128, 2, 4, 64, 3, 4, 4, 1
 #endif
 // few rows per expert (decode): LDS-staged weight stream with NS stages, K
 // walk rotated per workgroup, and (block decode form) pair lists built in the
