@@ -24,6 +24,16 @@ def rel_err(got, ref):
     return float(np.max(np.abs(got - ref)) / max(np.max(np.abs(ref)), 1e-30))
 
 
+def attn_part_err(got, ref, xm):
+    """Error of the attention part ``ref - xm`` relative to its largest value,
+    counted beyond the rounding of the stored bf16 output (8 significant bits:
+    at most 2^-8 |r_full| per element).  That rounding is set by r_full, which
+    the residual dominates, so without this allowance the bound could not be
+    met whenever the attention part is small next to the residual."""
+    excess = np.maximum(np.abs(got - ref) - 2.0 ** -8 * np.abs(ref), 0.0)
+    return float(np.max(excess) / max(np.max(np.abs(ref - xm)), 1e-30))
+
+
 def _run(inp):
     c = inp["cfg"]
     x = to_dev(inp["x"])
@@ -39,7 +49,7 @@ def _check(inp, got):
     ref, _ = ao.attention_block(inp["x"], inp["groups"], c["nq"], c["hd"], c["theta"], c["scale"])
     # the attention part alone as well (the residual dominates r_full)
     xm = inp["x"].astype(np.float64).mean(axis=0)
-    e_full, e_attn = rel_err(got, ref), rel_err(got - xm, ref - xm)
+    e_full, e_attn = rel_err(got, ref), attn_part_err(got, ref, xm)
     say(f"rel err r_full {e_full:.2e}, attention part {e_attn:.2e}")
     assert e_full <= TOL and e_attn <= TOL
 
@@ -86,7 +96,7 @@ def test_group_attention_full_size_sampled(name):
                                                     c["theta"], c["scale"], rows)
     ref /= c["H"]
     xm = x[:, rows].mean(axis=0)
-    e_full, e_attn = rel_err(got[rows], ref), rel_err(got[rows] - xm, ref - xm)
+    e_full, e_attn = rel_err(got[rows], ref), attn_part_err(got[rows], ref, xm)
     say(f"rel err r_full {e_full:.2e}, attention part {e_attn:.2e}")
     assert e_full <= TOL and e_attn <= TOL
 
@@ -149,6 +159,6 @@ def test_group_attention_long_sequence_sampled(nq, hd):
     ref = x[0, rows] + ao.group_attention_rows(x[0], g0["w_qkv"], g0["w_o"], cfg["nq"], cfg["hd"],
                                                cfg["theta"], cfg["scale"], rows)
     e_full = rel_err(got[rows], ref)
-    e_attn = rel_err(got[rows] - x[0, rows], ref - x[0, rows])
+    e_attn = attn_part_err(got[rows], ref, x[0, rows])
     say(f"rel err r_full {e_full:.2e}, attention part {e_attn:.2e}")
     assert e_full <= TOL and e_attn <= TOL
