@@ -101,8 +101,12 @@ def test_group_attention_full_size_sampled(name):
     assert e_full <= TOL and e_attn <= TOL
 
 
-def test_group_attention_deterministic_and_empty():
-    inp = synth.make_attention_inputs("attn_tiny_bf16")
+ONE_HEAD = dict(H=2, S=150, d=96, nq=1, hd=96, theta=500000.0, scale=16.0, sigma=0.05, seed=8)
+
+
+@pytest.mark.parametrize("cfg", ["attn_tiny_bf16", ONE_HEAD], ids=["two_heads", "one_head_hd96"])
+def test_group_attention_deterministic_and_empty(cfg):
+    inp = synth.make_attention_inputs(cfg)
     say("determinism")
     a = _run(inp)
     b = _run(inp)
@@ -114,10 +118,11 @@ def test_group_attention_deterministic_and_empty():
     assert e.shape == (0, 64)
 
 
-def test_group_attention_graph_replay():
+@pytest.mark.parametrize("cfg", ["attn_tiny_bf16", ONE_HEAD], ids=["two_heads", "one_head_hd96"])
+def test_group_attention_graph_replay(cfg):
     """The call captured in a HIP graph and replayed several times, with eager
     work between the replays, gives the eager result every time."""
-    inp = synth.make_attention_inputs("attn_tiny_bf16")
+    inp = synth.make_attention_inputs(cfg)
     c = inp["cfg"]
     x = to_dev(inp["x"])
     w_qkv = to_dev(np.stack([g["w_qkv"] for g in inp["groups"]]))
