@@ -426,6 +426,38 @@ def test_block_parity_shapes(T, d, E, k, F, C, scale, dt, bias):
     assert rel_err(got[~exempt], ref[~exempt]) <= TOL[dt]
 
 
+def _random_block_case(i):
+    """Shape i of a fixed pseudo-random set: dtype, clusters, tokens, widths,
+    experts, top-k, router bias and reduction scale all drawn."""
+    rng = np.random.default_rng([77, i])
+    dt = "f32" if rng.random() < 0.3 else "bf16"
+    C = int(rng.integers(1, 5))
+    T = int(rng.integers(1, 700 if dt == "bf16" else 200))
+    d = int(rng.integers(1, 49 if dt == "bf16" else 17)) * 8
+    E = int(rng.integers(1, 33))
+    k = int(rng.integers(1, min(E, 4) + 1))
+    F = int(rng.integers(1, 41 if dt == "bf16" else 17)) * 8
+    bias = "zipf1.2" if rng.random() < 0.5 else None
+    scale = None if rng.random() < 0.5 else float(rng.choice([0.5, 1.0]))
+    return dict(dtype=dt, C=C, T=T, d=d, E=E, k=k, F=F, sigma=0.05, seed=2000 + i,
+                bias=bias), scale
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_block_parity_random_shapes(i):
+    cfg, scale = _random_block_case(i)
+    say("block random shape", i, cfg, scale)
+    inp = synth.make_block_inputs(cfg)
+    got = _block_gpu(inp, scale)
+    ref, res = oracle.cluster_block(inp["x"], inp["clusters"], cfg["k"], scale)
+    exempt = np.zeros(cfg["T"], dtype=bool)
+    for r in res:
+        exempt |= r["margin"] < EXEMPT
+    assert np.all(np.isfinite(got))
+    if (~exempt).any():
+        assert rel_err(got[~exempt], ref[~exempt]) <= TOL[cfg["dtype"]]
+
+
 @pytest.mark.parametrize("T,d,E,k,F,C", [
     (128, 256, 16, 2, 128, 1),  # decode form, one cluster
     (96, 128, 8, 2, 64, 3),     # three clusters, one score matrix
