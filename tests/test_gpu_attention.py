@@ -78,6 +78,20 @@ def test_group_attention_parity(H, S, d, nq, hd, theta, scale):
     _check(inp, _run(inp))
 
 
+@pytest.mark.parametrize("i", range(8))
+def test_group_attention_random_shapes(i):
+    """Shape i of a fixed pseudo-random set (groups, length, width, query heads
+    per group, head size, rotary base and scale), in full against the oracle."""
+    rng = np.random.default_rng([55, i])
+    cfg = dict(H=int(rng.integers(1, 4)), S=int(rng.integers(1, 700)),
+               d=int(rng.integers(1, 33)) * 8, nq=int(rng.integers(1, 5)),
+               hd=int(rng.choice([96, 128])), theta=float(rng.choice([1e4, 5e5])),
+               scale=float(rng.choice([1.0, 16.0])), sigma=0.05, seed=3000 + i)
+    say("random shape", i, cfg)
+    inp = synth.make_attention_inputs(cfg)
+    _check(inp, _run(inp))
+
+
 @pytest.mark.parametrize("name", ["attn_share_bf16", "attn_small_bf16"])
 def test_group_attention_full_size_sampled(name):
     """The 8-group, 4096-token configurations of the 7B (hd = 128, two query
