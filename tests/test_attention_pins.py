@@ -122,3 +122,30 @@ def test_attention_inputs_are_seeded_and_bf16():
     assert np.array_equal(a["groups"][1]["w_qkv"], b["groups"][1]["w_qkv"])
     for t in (a["x"], a["groups"][0]["w_qkv"], a["groups"][0]["w_o"]):
         assert np.array_equal(t, synth.round_to_bf16(t))
+
+
+@pytest.mark.parametrize("hd,nq,theta,scale,S", [
+    (128, 2, 500000.0, 16.0, 300),
+    (128, 1, 10000.0, 1.0, 129),
+    (96, 1, 500000.0, 16.0, 257),
+    (96, 3, 10000.0, 16.0, 64),
+    (128, 3, 500000.0, 1.0, 97),
+    (96, 2, 10000.0, 1.0, 1),
+])
+def test_rows_form_equals_whole_sequence_form(hd, nq, theta, scale, S):
+    """``group_attention_rows`` (the reference of the full-size sampled checks)
+    agrees with the pinned ``group_attention`` at every query position: a wrong
+    per-row rotary angle, causal bound or head slice there would fail here."""
+    rng = np.random.default_rng([hd, nq, S])
+    d = 40
+    x = rng.standard_normal((S, d))
+    w_qkv = rng.standard_normal(((nq + 2) * hd, d)) * 0.15
+    w_o = rng.standard_normal((d, nq * hd)) * 0.15
+    whole, _ = ao.group_attention(x, w_qkv, w_o, nq, hd, theta, scale)
+    rows = np.arange(S)
+    part = ao.group_attention_rows(x, w_qkv, w_o, nq, hd, theta, scale, rows)
+    assert np.max(np.abs(part - whole)) <= 1e-12 * max(1.0, np.max(np.abs(whole)))
+    # an unordered subset (first, last, interior) gives the same rows
+    sub = np.unique(np.array([S - 1, 0, S // 2, S // 3]))[::-1]
+    part2 = ao.group_attention_rows(x, w_qkv, w_o, nq, hd, theta, scale, sub)
+    assert np.max(np.abs(part2 - whole[sub])) <= 1e-12 * max(1.0, np.max(np.abs(whole)))

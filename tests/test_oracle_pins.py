@@ -68,6 +68,60 @@ def test_topk_integer_ties_max_sum(E, k):
     assert np.any(margin == 0)  # ties at the boundary do occur here
 
 
+def _bruteforce_gaps(g32_row, k):
+    """Margin and smallest adjacent gap among the top k, by sorting the fp32
+    scores of one token with Python's ``sorted`` on (score desc, id asc)."""
+    vals = [float(v) for v in g32_row]
+    order = sorted(range(len(vals)), key=lambda e: (-vals[e], e))
+    top = [vals[e] for e in order[:k]]
+    margin = vals[order[k - 1]] - vals[order[k]] if k < len(vals) else math.inf
+    gaps = [top[a] - top[a + 1] for a in range(k - 1)]
+    return margin, (min(gaps) if gaps else math.inf)
+
+
+@pytest.mark.parametrize("E,k,kind", [(8, 1, "normal"), (8, 3, "normal"), (16, 2, "normal"),
+                                      (6, 6, "normal"), (8, 4, "ties"), (5, 1, "ties"),
+                                      (7, 3, "near")])
+def test_margin_and_min_gap_bruteforce(E, k, kind):
+    """``margin`` and ``min_gap`` (which decide where ids and slot order are
+    compared) against a per-token sort; exact ties give a zero gap, k = 1 no
+    gap, k = E no margin."""
+    rng = np.random.default_rng([E, k, len(kind)])
+    if kind == "ties":
+        g = rng.integers(-2, 3, size=(300, E)).astype(np.float64)
+    elif kind == "near":
+        # pairs of scores a few fp32 ulps apart, and pairs equal in fp32 but
+        # not in fp64
+        g = rng.standard_normal((300, E))
+        g[:, 1] = np.nextafter(np.float32(g[:, 0]), np.float32(np.inf)).astype(np.float64)
+        g[:100, 2] = g[:100, 0] + 1e-12
+    else:
+        g = rng.standard_normal((300, E))
+    _, margin, min_gap = oracle.topk_select(g, k)
+    g32 = g.astype(np.float32)
+    for t in range(g.shape[0]):
+        m, mg = _bruteforce_gaps(g32[t], k)
+        assert margin[t] == m and min_gap[t] == mg, t
+    if kind == "ties" and k > 1:
+        assert np.any(min_gap == 0.0)
+    if k == 1:
+        assert np.all(np.isinf(min_gap))
+    if k == E:
+        assert np.all(np.isinf(margin))
+
+
+@pytest.mark.parametrize("name", ["decode_bf16", "prefill_zipf_bf16", "layer_share_bf16"])
+def test_slot_order_check_is_not_vacuous(name):
+    """On the seeded workloads nearly every token has all adjacent top-k gaps
+    and its k/(k+1) margin above the 1e-5 exemption, so the slot-order and id
+    comparisons cover nearly all tokens (first 2048 tokens, every cluster)."""
+    inp = synth.make_block_inputs(name, T=2048)
+    for cl in inp["clusters"]:
+        r = oracle.route(inp["x"], cl["w_router"], cl["bias"], inp["cfg"]["k"])
+        assert np.mean(r["min_gap"] >= 1e-5) > 0.99
+        assert np.mean(r["margin"] >= 1e-5) > 0.99
+
+
 def test_topk_decided_in_fp32():
     """Scores that differ only below fp32 resolution are a tie -> lower id."""
     g = np.array([[1.0, 1.0 + 1e-12, 0.0], [0.5, 0.5 - 1e-13, 0.7]])
