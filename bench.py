@@ -5,11 +5,18 @@ One step = one foe_cluster_block call (route -> permute -> grouped SwiGLU FFN
 already resident in HBM.  Prints ONE JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--config NAME]
-                  [--no-graph] [--cpu-seconds S]
+                  [--only] [--no-graph] [--cpu-seconds S]
 
-Default workload: the decode-shaped cluster block (T=128, d=2048, E=16, k=2,
-F=1024, bf16).  Several independent weight/input sets are rotated so the
-working set exceeds the 256 MB Infinity Cache.
+Headline workload: the prefill-shaped cluster block with Zipf(1.2) router skew
+(T=8192, d=2048, E=16, k=2, F=1024, bf16), where the expert FFN is bound by
+the matrix cores.  The same line nests, under "workloads", one record per
+other block workload -- decode (T=128, weight-streaming bound), large
+(T=16384, d=4096, E=32, k=4, F=1536) and the 8-cluster layer share (C=8,
+T=4096, E=8) -- each with its step time, tokens/s, expert-FFN TFLOP/s, the
+roofline object of its dominant kernel and per-kernel fractions.  `--only`
+(or any `--config`) measures the named workload alone.  Several independent
+weight/input sets are rotated where one set is smaller than twice the
+256 MB Infinity Cache.
 
 `--config attn_share_bf16` (or another attention configuration) times the
 per-group attention that feeds the block instead: one step = one
@@ -22,7 +29,8 @@ counters read for a plain copy of known size: `--copy-calibration`), read from
 profiles/traffic.json; it is null when no measurement exists for this
 workload or the kernel's source has changed since it was taken.
 
-Timed passes (both over K steps, HIP events on the library's stream):
+Timed passes per workload (both over K steps, HIP events on the library's
+stream):
   A  plain steps, launched eagerly and (unless --no-graph) replayed from HIP
      graphs -> value / ms_per_step from the faster of the two (both times
      are reported; config.launch names the one used)
@@ -47,7 +55,9 @@ METRIC = "tokens/s and expert-FFN TFLOP/s per FoE cluster block (decode & prefil
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
 FP32_VALU_PEAK_TFLOPS = 157.3   # fp32 vector
-DEFAULT_CONFIG = "decode_bf16"
+DEFAULT_CONFIG = "prefill_zipf_bf16"
+# measured after the headline, in the same JSON line
+NESTED_WORKLOADS = ("decode_bf16", "large_bf16", "layer_share_bf16")
 MALL_BYTES = 256 << 20
 
 
@@ -56,7 +66,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default=DEFAULT_CONFIG)
+    ap.add_argument("--config", default=None,
+                    help=f"workload (default {DEFAULT_CONFIG} plus the nested block workloads)")
+    ap.add_argument("--only", action="store_true",
+                    help="measure the headline workload alone (no nested records)")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the oracle CPU baseline (0 = skip)")
@@ -393,12 +406,38 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    args.nested = args.config is None and not args.only
+    if args.config is None:
+        args.config = DEFAULT_CONFIG
     if args.config in synth.ATTN_CONFIGS:
         main_attention(args)
         return
     torch.cuda.set_device(0)
+    line = run_block(args, args.config)
+    if args.nested:
+        line["workloads"] = {}
+        for name in NESTED_WORKLOADS:
+            torch.cuda.empty_cache()
+            rec = run_block(args, name)
+            line["workloads"][name] = {key: rec[key] for key in (
+                "value", "unit", "ms_per_step", "dtype", "config", "block_tflops",
+                "expert_ffn_tflops", "eager_ms_per_step", "graph_ms_per_step",
+                "profiled_ms_per_step", "roofline", "kernels")}
+    if args.cpu_seconds > 0:
+        line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+def run_block(args, name):
+    """Passes A and B of one block workload; returns its record (no CPU
+    baseline)."""
+    import numpy as np
+    import torch
+
+    from paper_2605_06206_amd import foe, synth
+
     dev = "cuda:0"
-    cfg = dict(synth.CONFIGS[args.config], name=args.config)
+    cfg = dict(synth.CONFIGS[name], name=name)
     dt = cfg["dtype"]
     T, d, E, k, F, C = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["F"], cfg["C"]
     s_el = 2 if dt == "bf16" else 4
@@ -412,7 +451,7 @@ def main():
 
     sets = []
     for i in range(nsets):
-        inp = synth.make_block_inputs(args.config, weight_set=i)
+        inp = synth.make_block_inputs(name, weight_set=i)
         cls = inp["clusters"]
         st = {"x": up(inp["x"])}
         for key in ("w_router", "w_gate", "w_up", "w_down"):
@@ -488,7 +527,7 @@ def main():
     t_b, kernels = kernel_profile(foe, args.steps, lambda n: timed(n, lambda i: step(i, sraw)))
     dom = max(kernels, key=lambda n: kernels[n]["total_ms"])
     roof = roofline(dom, cfg, e_touched, kernels[dom]["avg_us"] * 1e-6)
-    roof["traffic"] = measured_traffic(args.config, dom)
+    roof["traffic"] = measured_traffic(name, dom)
     per_kernel_roof = {n: roofline(n, cfg, e_touched, v["avg_us"] * 1e-6)
                        for n, v in kernels.items() if kernel_work(n, cfg, e_touched)[1] > 0}
 
@@ -509,7 +548,7 @@ def main():
         "dtype": dt,
         "data": "synthetic (seeded N(0,1) activations, N(0,sigma) weights; "
                 f"{nsets} rotated input/weight sets)",
-        "config": {"workload": f"{args.config}: C={C} T={T} d={d} E={E} k={k} F={F} {dt}",
+        "config": {"workload": f"{name}: C={C} T={T} d={d} E={E} k={k} F={F} {dt}",
                    "C": C, "T": T, "d": d, "E": E, "k": k, "F": F,
                    "launch": "hip_graph_replay" if use_graph else "eager"},
         "block_tflops": round(flops / (ms * 1e-3) / 1e12, 3),
@@ -524,9 +563,10 @@ def main():
                     for n, v in kernels.items()},
         "cpu_baseline": None,
     }
-    if args.cpu_seconds > 0:
-        line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_seconds)
-    print(json.dumps(line), flush=True)
+    del sets, calls, ws, out
+    return line
+
+
 
 
 if __name__ == "__main__":
