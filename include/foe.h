@@ -230,6 +230,32 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
                          void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * foe_cluster_block_noalloc - foe_cluster_block (FOE_GATE_RENORM) for callers
+ * that cannot allocate device memory or pass a workspace: code under HIP-graph
+ * capture, tight serving loops, harnesses that forbid allocation.  Same
+ * arguments as foe_cluster_block without ws / ws_bytes, same kernels, same
+ * results bit for bit.
+ *
+ * Its scratch is a static device array of the library, one copy per GPU,
+ * reserved when the library's code is first loaded on that GPU and held until
+ * the process ends.  Its size is 128 MiB (134217728 bytes): enough for the
+ * decode- and prefill-shaped blocks, e.g. C=1, T=8192, d=2048, E=16, k=2,
+ * F=1024.  Sizes whose workspace
+ * (foe_workspace_bytes("cluster_block", ...)) exceeds it are rejected with
+ * FOE_ERR_UNSUPPORTED before anything is enqueued.  The call allocates no
+ * device or host memory.
+ *
+ * Every call on one GPU uses that GPU's one array, which keeps the last call's
+ * contents (the block clears what it needs itself): calls that overlap on one
+ * GPU (two host threads, or two streams without an ordering between them)
+ * race and give undefined results.  Calls ordered on one stream are safe.
+ */
+int foe_cluster_block_noalloc(foe_dtype dt, int C, int T, int d, int E, int k, int F,
+                              const void* x, const void* w_router, const float* bias,
+                              const void* w_gate, const void* w_up, const void* w_down,
+                              float reduce_scale, void* out, void* stream);
+
+/*
  * foe_group_attention - the per-group attention that feeds the block (Table 3,
  * FoE column, rows "Attn. residual" and "Cross-group avg."):
  *   r[h,i]    = x[h,i] + Attn_h(x[h,:])[i]     (every group its own representation)

@@ -146,6 +146,39 @@ int& profile_cur_slot() {
 
 }  // namespace foe
 
+// ---- scratch of the entry point that allocates nothing ---------------------
+// One copy per GPU the library runs on, held until the process ends.  Host
+// code never uses the array's name as an address: the device address of each
+// GPU's copy comes from hipGetSymbolAddress, taken once per device with that
+// device current.
+constexpr size_t kNoAllocScratchBytes = (size_t)128 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace foe {
+namespace {
+std::mutex g_scratch_mu;
+std::vector<void*> g_scratch_ptr;  // per device ordinal; null until first taken
+
+// Device address of the current device's scratch array.
+int noalloc_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "foe_cluster_block_noalloc/hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if ((size_t)dev >= g_scratch_ptr.size()) g_scratch_ptr.resize((size_t)dev + 1, nullptr);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "foe_cluster_block_noalloc/hipGetSymbolAddress");
+    if (p == nullptr) return fail(FOE_ERR_HIP, "foe_cluster_block_noalloc: no scratch address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return FOE_OK;
+}
+}  // namespace
+}  // namespace foe
+
 using namespace foe;
 
 extern "C" {
@@ -341,11 +374,15 @@ int foe_cluster_block(foe_dtype dt, int C, int T, int d, int E, int k, int F, co
                               w_up, w_down, reduce_scale, out, ws, ws_bytes, stream);
 }
 
-int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
-                         foe_gating gating, const void* x, const void* w_router,
-                         const float* bias, const void* w_gate, const void* w_up,
-                         const void* w_down, float reduce_scale, void* out, void* ws,
-                         size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace foe {
+namespace {
+// Argument checks of the whole block (every pointer and size; nothing is
+// enqueued).  Returns FOE_OK or the status to report, with the message set.
+int check_block_args(const char* who, foe_dtype dt, int C, int T, int d, int E, int k, int F,
+                     foe_gating gating, const void* x, const void* w_router, const float* bias,
+                     const void* w_gate, const void* w_up, const void* w_down, const void* out) {
   Check c;
   c.need(gating == FOE_GATE_RENORM || gating == FOE_GATE_GLOBAL,
          "gating must be FOE_GATE_RENORM or FOE_GATE_GLOBAL");
@@ -363,15 +400,33 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
   c.tensor(w_up, any, "w_up");
   c.tensor(w_down, any, "w_down");
   c.tensor(out, any, "out");
-  if (!c.err.empty()) return fail(FOE_ERR_INVALID, "foe_cluster_block: " + c.err);
+  if (!c.err.empty()) return fail(FOE_ERR_INVALID, std::string(who) + ": " + c.err);
   if (gating == FOE_GATE_GLOBAL && !route_one_pass(C, E))
     return fail(FOE_ERR_UNSUPPORTED,
-                "foe_cluster_block: global gating needs C == 1 or C*E <= 256");
-  if (!any) return FOE_OK;
+                std::string(who) + ": global gating needs C == 1 or C*E <= 256");
   const long long CR = (long long)C * T * k;
-  if (dt == FOE_BF16 && !(operand_fits(T, d, 2) && operand_fits(CR, F, 2) && operand_fits(CR, d, 2)))
-    return fail(FOE_ERR_UNSUPPORTED,
-                "foe_cluster_block: T*d, C*T*k*F and C*T*k*d must stay below 2^30 bf16 elements");
+  if (any && dt == FOE_BF16 &&
+      !(operand_fits(T, d, 2) && operand_fits(CR, F, 2) && operand_fits(CR, d, 2)))
+    return fail(FOE_ERR_UNSUPPORTED, std::string(who) +
+                                         ": T*d, C*T*k*F and C*T*k*d must stay below 2^30 "
+                                         "bf16 elements");
+  return FOE_OK;
+}
+}  // namespace
+}  // namespace foe
+
+extern "C" {
+
+int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
+                         foe_gating gating, const void* x, const void* w_router,
+                         const float* bias, const void* w_gate, const void* w_up,
+                         const void* w_down, float reduce_scale, void* out, void* ws,
+                         size_t ws_bytes, void* stream) {
+  const int rc = check_block_args("foe_cluster_block", dt, C, T, d, E, k, F, gating, x, w_router,
+                                  bias, w_gate, w_up, w_down, out);
+  if (rc != FOE_OK) return rc;
+  if (T == 0) return FOE_OK;
+  const long long CR = (long long)C * T * k;
   const BlockWs L = block_ws(dt, C, T, d, E, k, F);
   if (ws == nullptr || !aligned16(ws))
     return fail(FOE_ERR_INVALID, "foe_cluster_block: ws is NULL or not 16-byte aligned");
@@ -430,6 +485,27 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
   e = launch_combine_clusters(dt, C, T, d, k, y, row_of, topk_w, x, reduce_scale, out, s);
   if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/combine");
   return FOE_OK;
+}
+
+int foe_cluster_block_noalloc(foe_dtype dt, int C, int T, int d, int E, int k, int F,
+                              const void* x, const void* w_router, const float* bias,
+                              const void* w_gate, const void* w_up, const void* w_down,
+                              float reduce_scale, void* out, void* stream) {
+  const int rc = check_block_args("foe_cluster_block_noalloc", dt, C, T, d, E, k, F,
+                                  FOE_GATE_RENORM, x, w_router, bias, w_gate, w_up, w_down, out);
+  if (rc != FOE_OK) return rc;
+  const size_t need = block_ws(dt, C, T, d, E, k, F).total;
+  if (need > kNoAllocScratchBytes)
+    return fail(FOE_ERR_UNSUPPORTED,
+                "foe_cluster_block_noalloc: these sizes need " + std::to_string(need) +
+                    " bytes of scratch; the entry point holds at most " +
+                    std::to_string(kNoAllocScratchBytes) + " (use foe_cluster_block)");
+  if (T == 0) return FOE_OK;
+  void* ws = nullptr;
+  const int rs = noalloc_scratch(&ws);
+  if (rs != FOE_OK) return rs;
+  return foe_cluster_block_ex(dt, C, T, d, E, k, F, FOE_GATE_RENORM, x, w_router, bias, w_gate,
+                              w_up, w_down, reduce_scale, out, ws, kNoAllocScratchBytes, stream);
 }
 
 size_t foe_group_attention_workspace_bytes(int H, int S, int d, int nq, int hd) {

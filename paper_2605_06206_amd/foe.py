@@ -45,6 +45,8 @@ _SIGNATURES = {
     "foe_cluster_block_ex": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
                                       _c_int, _p, _p, _p, _p, _p, _p, _c_float, _p, _p, _c_size,
                                       _p]),
+    "foe_cluster_block_noalloc": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                           _c_int, _p, _p, _p, _p, _p, _p, _c_float, _p, _p]),
     "foe_workspace_bytes": (_c_size, [ctypes.c_char_p, _c_int, _c_int, _c_int, _c_int, _c_int,
                                       _c_int, _c_int]),
     "foe_group_attention": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_float,
@@ -257,6 +259,28 @@ def cluster_block(x, w_router, bias, w_gate, w_up, w_down, k, reduce_scale=None,
     else:
         _check(lib().foe_cluster_block_ex(dt, C, T, d, E, k, F, _gating(gating), *args),
                "foe_cluster_block_ex")
+    return out
+
+
+# bytes of the per-GPU scratch array of foe_cluster_block_noalloc
+NOALLOC_SCRATCH_BYTES = 128 << 20
+
+
+def cluster_block_noalloc(x, w_router, bias, w_gate, w_up, w_down, k, reduce_scale=None,
+                          out=None, stream=None):
+    """foe_cluster_block_noalloc: foe_cluster_block without a workspace (the
+    library's per-GPU scratch array); weights stacked on a leading C axis."""
+    T, d = x.shape
+    C, E, F, _ = w_gate.shape
+    if reduce_scale is None:
+        reduce_scale = 1.0 / C
+    if out is None:
+        out = torch.empty((T, d), dtype=x.dtype, device=x.device)
+    _check(lib().foe_cluster_block_noalloc(
+        _dt(x), C, T, d, E, k, F, _dev(x, "x"), _dev(w_router, "w_router", x.dtype),
+        _dev(bias, "bias", torch.float32), _dev(w_gate, "w_gate", x.dtype),
+        _dev(w_up, "w_up", x.dtype), _dev(w_down, "w_down", x.dtype), float(reduce_scale),
+        _dev(out, "out", x.dtype), _stream(stream)), "foe_cluster_block_noalloc")
     return out
 
 

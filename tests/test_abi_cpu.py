@@ -190,6 +190,25 @@ def test_cluster_block_rejects(L):
                                ctypes.c_float(0.125), None, None, 0, None) == foe.FOE_OK
 
 
+def test_cluster_block_noalloc_rejects_on_the_host(L):
+    """Sizes past the scratch array and bad arguments are refused before any
+    device call (these run without a GPU)."""
+    f = ctypes.c_float(0.125)
+    cap = foe.NOALLOC_SCRATCH_BYTES
+    # the prefill-shaped block fits, the large one does not
+    assert L.foe_workspace_bytes(b"cluster_block", BF16, 1, 8192, 2048, 16, 2, 1024) <= cap
+    assert L.foe_workspace_bytes(b"cluster_block", BF16, 1, 16384, 4096, 32, 4, 1536) > cap
+    big = [BF16, 1, 16384, 4096, 32, 4, 1536, P, P, None, P, P, P, f, P, None]
+    assert L.foe_cluster_block_noalloc(*big) == foe.FOE_ERR_UNSUPPORTED
+    assert "bytes of scratch" in foe.last_error() and str(cap) in foe.last_error()
+    bad = [BF16, 1, 128, 2048, 16, 2, 1024, None, P, None, P, P, P, f, P, None]
+    assert L.foe_cluster_block_noalloc(*bad) == INV and "x is NULL" in foe.last_error()
+    bad = [BF16, 1, 128, 2048, 16, 17, 1024, P, P, None, P, P, P, f, P, None]
+    assert L.foe_cluster_block_noalloc(*bad) == INV and "k must" in foe.last_error()
+    assert L.foe_cluster_block_noalloc(BF16, 1, 0, 2048, 16, 2, 1024, None, None, None, None,
+                                       None, None, f, None, None) == foe.FOE_OK
+
+
 def test_workspace_bytes(L):
     for op in (b"route", b"combine", b"reduce"):
         assert L.foe_workspace_bytes(op, BF16, 1, 128, 64, 4, 2, 64) == 0
