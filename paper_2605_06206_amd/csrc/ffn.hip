@@ -227,25 +227,57 @@ struct GemmResid {
   float scale = 1.f;
 };
 
-template <int BM, int BN, int WM, int WN, bool GATEUP, int BK, int NST, int PW, int GM,
-          int PERSIST, bool RESID = false>
-__global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1, 2)))
-void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv,
-                      int a_rows, const int32_t* __restrict__ offsets, int E, int rows,
-                      const bf16* __restrict__ B0, const bf16* __restrict__ B1, int N, int K,
-                      bf16* __restrict__ out, int n_tiles_n, int n_tiles, GemmResid res) {
+// Operands of one grouped GEMM: A rows (direct, or gathered as gather[r] /
+// kdiv from a_rows source rows), one or two [E, N, K] weight stacks, the
+// output [rows, N] (out_bytes = its size, for device-scope stores) and the
+// residual epilogue.
+struct GemmArgs {
+  const bf16* A;
+  const int32_t* gather;
+  int kdiv;
+  int a_rows;
+  const bf16* B0;
+  const bf16* B1;
+  int N;
+  int K;
+  bf16* out;
+  uint32_t out_bytes;
+  GemmResid res;
+  // two-matrix tile shape (GATEUP) used for a plain product: B1 is ignored,
+  // and the tile's two BN-row weight slices are rows ntile*2*BN .. +BN and
+  // .. +2*BN of B0, stored side by side (no SwiGLU); the tile covers 2*BN
+  // output columns
+  bool halves;
+};
+
+// One BM x BN output tile of expert e (rows row0 .. row_end-1, N-tile ntile)
+// over all of K, staged through the workgroup's LDS `smem`.  OUT_CPOL = 0
+// stores the output tile through the caches as usual; otherwise the stores
+// carry that cache policy (kScDevice: written through past the XCD's L2, so
+// that other XCDs can read the tile once the stores have completed).  The
+// two-slice form (GemmArgs::halves) always stores as usual.
+template <int BM, int BN, int WM, int WN, bool GATEUP, int BK, int NST, int PW, bool RESID,
+          int OUT_CPOL>
+__device__ __forceinline__ void gemm_tile(unsigned char* smem, const GemmArgs& g, const int e,
+                                          const int row0, const int row_end, const int ntile,
+                                          int32_t* signal = nullptr) {
   static_assert(!(RESID && GATEUP), "residual epilogue on the plain form only");
   using C = DmaCfg<BM, BN, WM, WN, GATEUP, BK, NST, PW>;
   constexpr int NLD = C::NLD;
-  __shared__ __align__(1024) unsigned char smem[NST * C::STAGE];
+  const bf16* __restrict__ A = g.A;
+  const int32_t* __restrict__ gather = g.gather;
+  const int kdiv = g.kdiv, a_rows = g.a_rows, N = g.N, K = g.K;
+  const bf16* __restrict__ B0 = g.B0;
+  const bf16* __restrict__ B1 = g.B1;
+  bf16* __restrict__ out = g.out;
+  const GemmResid& res = g.res;
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-
-  auto run_tile = [&](const int e, const int row0, const int row_end, const int ntile) {
+  {
     const int n0 = ntile * BN;
 
     const int n_valid = min(BN, N - n0);
@@ -261,6 +293,14 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
     if constexpr (GATEUP) {
       t_base[2] = B1 + ((size_t)e * N + n0) * K;
       t_bytes[2] = t_bytes[1];
+      if (g.halves) {
+        // the two slices of a 2*BN-column tile of B0 (a slice past N is empty)
+        const int h0 = ntile * 2 * BN, h1 = min(h0 + BN, N);
+        t_base[1] = B0 + ((size_t)e * N + h0) * K;
+        t_bytes[1] = (uint32_t)max(min(BN, N - h0), 0) * K * 2u;
+        t_base[2] = B0 + ((size_t)e * N + h1) * K;
+        t_bytes[2] = (uint32_t)max(min(BN, N - h1), 0) * K * 2u;
+      }
     }
 
     // DMA instruction gq of a stage covers RPI rows (1 KiB) of the A tile
@@ -436,6 +476,13 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
           for (int q = 0; q < NLD; ++q) issue_one(st, st, q);
       }
       vm_barrier<NLD * (NST - 2)>();
+      // `signal`: counted once every wave's earlier stores have completed
+      // (with two stages the wait above drains every earlier memory
+      // operation of the wave, and the barrier meets all waves)
+      if (signal != nullptr) {
+        if constexpr (NST != 2) vm_barrier<0>();
+        if (threadIdx.x == 0) atomicAdd(signal, 1);
+      }
       fload(0, 0, 0);
       for (int kt = 0; kt < nk; kt += NST) {
 #pragma unroll
@@ -450,6 +497,7 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
       k_loop(std::false_type{});
 
     // epilogue: lane holds row m = .. + lane%32, columns n = .. + 8q + 4*(lane/32) + [0,4)
+    [[maybe_unused]] const __amdgpu_buffer_rsrc_t out_rsrc = make_rsrc_u(out, g.out_bytes);
     if constexpr (RESID) {
       // the residual added to the accumulators, the loads of all of the
       // lane's outputs in flight together
@@ -475,6 +523,74 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
 #pragma unroll
             for (int v = 0; v < 4; ++v) acc[0][i][j][q * 4 + v] += xv[i][j][q][v];
     }
+    if constexpr (GATEUP && OUT_CPOL != 0) {
+      if (!g.halves) {
+        // Device-scope stores of whole lines: the SwiGLU tile goes to LDS
+        // first (free after the K loop; 16-byte chunk c of tile row r at slot
+        // c ^ (r & 15), so the writes of 16 rows at one chunk spread over the
+        // banks), then every lane stores 16-byte chunks of whole rows (a wave
+        // instruction covers 4 rows of 256 bytes), so the stores that pass
+        // the L2 are full 128-byte lines rather than 16-byte pieces of 32.
+        static_assert(BN == 128, "16 chunks per staged row");
+        constexpr int ORB = BN * 2;
+#pragma unroll
+        for (int i = 0; i < C::SM; ++i) {
+          const int rr = wm * C::WTM + i * 32 + lrow;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int ch = (wn * C::WTN + q * 8) / 8;
+            bf16x4 o;
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+              o[v] = (bf16)(silu_f(acc[0][i][0][q * 4 + v]) * acc[1][i][0][q * 4 + v]);
+            *reinterpret_cast<bf16x4*>(smem + rr * ORB + ((ch ^ (rr & 15)) * 16) +
+                                       (lane >> 5) * 8) = o;
+          }
+        }
+        lds_barrier();
+        constexpr int NCH = BM * (BN / 8);
+        static_assert(NCH % C::NTHR == 0, "whole store rounds");
+#pragma unroll
+        for (int k = 0; k < NCH / C::NTHR; ++k) {
+          const int c = tid + k * C::NTHR;
+          const int rr = c / (BN / 8), ch = c % (BN / 8);
+          const int m = row0 + rr, n = n0 + ch * 8;
+          if (m < row_end && n < N) {
+            const bf16x8 o =
+                *reinterpret_cast<const bf16x8*>(smem + rr * ORB + ((ch ^ (rr & 15)) * 16));
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o), out_rsrc,
+                                                   (uint32_t)(((size_t)m * N + n) * 2), 0,
+                                                   OUT_CPOL);
+          }
+        }
+        return;
+      }
+    }
+    if constexpr (GATEUP) {
+      if (g.halves) {
+        // slice b of the tile: columns ntile*2*BN + b*BN + ..
+#pragma unroll
+        for (int i = 0; i < C::SM; ++i) {
+          const int m = row0 + wm * C::WTM + i * 32 + lrow;
+          if (m >= row_end) continue;
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int j = 0; j < C::SN; ++j)
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int n = ntile * 2 * BN + b * BN + wn * C::WTN + j * 32 + q * 8 +
+                              (lane >> 5) * 4;
+                if (n >= N) continue;
+                bf16x4 o;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) o[v] = (bf16)acc[b][i][j][q * 4 + v];
+                *reinterpret_cast<bf16x4*>(out + (size_t)m * N + n) = o;
+              }
+        }
+        return;
+      }
+    }
 #pragma unroll
     for (int i = 0; i < C::SM; ++i) {
       const int m = row0 + wm * C::WTM + i * 32 + lrow;
@@ -498,29 +614,55 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
           bf16x4 o;
 #pragma unroll
           for (int v = 0; v < 4; ++v) o[v] = (bf16)val[v];
-          *reinterpret_cast<bf16x4*>(out + (size_t)m * N + n) = o;
+          if constexpr (OUT_CPOL != 0)
+            __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, o), out_rsrc,
+                                                  (uint32_t)(((size_t)m * N + n) * 2), 0,
+                                                  OUT_CPOL);
+          else
+            *reinterpret_cast<bf16x4*>(out + (size_t)m * N + n) = o;
         }
       }
     }
+  }
+}
+
+// tile t -> (M-tile, N-tile) of m_tiles x ntn tiles: groups of GM M-tiles are
+// walked N-tile by N-tile, so that a run of consecutive tiles shares A rows
+// and weight slices
+template <int GM>
+__device__ __forceinline__ void tile_coords(int t, int ntn, int m_tiles, int& mt, int& nt) {
+  if constexpr (GM <= 1) {
+    mt = t / ntn;
+    nt = t % ntn;
+  } else {
+    // the last group may hold fewer than GM M-tiles
+    const int grp = t / (GM * ntn), i = t % (GM * ntn);
+    const int g = min(GM, m_tiles - grp * GM);
+    mt = grp * GM + i % g;
+    nt = i / g;
+  }
+}
+
+template <int BM, int BN, int WM, int WN, bool GATEUP, int BK, int NST, int PW, int GM,
+          int PERSIST, bool RESID = false>
+__global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1, 2)))
+void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv,
+                      int a_rows, const int32_t* __restrict__ offsets, int E, int rows,
+                      const bf16* __restrict__ B0, const bf16* __restrict__ B1, int N, int K,
+                      bf16* __restrict__ out, int n_tiles_n, int n_tiles, GemmResid res) {
+  using C = DmaCfg<BM, BN, WM, WN, GATEUP, BK, NST, PW>;
+  __shared__ __align__(1024) unsigned char smem[NST * C::STAGE];
+  const GemmArgs g{A, gather, kdiv, a_rows, B0, B1, N, K, out, 0u, res, false};
+  auto run_tile = [&](const int e, const int row0, const int row_end, const int ntile) {
+    gemm_tile<BM, BN, WM, WN, GATEUP, BK, NST, PW, RESID, 0>(smem, g, e, row0, row_end, ntile);
   };
 
   // M-tiles that hold rows (persistent form: the tile list is split over
   // the XCDs by this count, not by the launch's upper bound)
   const int m_tiles = PERSIST ? __builtin_amdgcn_readfirstlane(total_mtiles(offsets, E, rows, BM))
                               : n_tiles / n_tiles_n;
-  // tile t -> (M-tile, N-tile): groups of GM M-tiles are walked N-tile by
-  // N-tile, so that a run of consecutive tiles shares A rows and weight slices
   auto tile_coords = [&](int t, int& mt, int& nt) {
-    if constexpr (GM <= 1) {
-      mt = t / n_tiles_n;
-      nt = t % n_tiles_n;
-    } else {
-      // the last group may hold fewer than GM M-tiles
-      const int grp = t / (GM * n_tiles_n), i = t % (GM * n_tiles_n);
-      const int g = min(GM, m_tiles - grp * GM);
-      mt = grp * GM + i % g;
-      nt = i / g;
-    }
+    foe::tile_coords<GM>(t, n_tiles_n, m_tiles, mt, nt);
   };
   auto run_t = [&](int t) {
     int mt, nt, e, row0, row_end;
@@ -556,6 +698,122 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
     if (!find_tile(offsets, E, rows, BM, mt, e, row0, row_end)) return;
     run_tile(e, row0, row_end, nt);
   }
+}
+
+// Both grouped GEMMs of the expert FFN in one persistent launch.  Work items
+// are the gate/up tiles (SwiGLU epilogue, writing h) followed by the down
+// tiles (reading h, writing y), numbered in that order and handed out one at a
+// time from a device-side counter, so the two GEMMs share one schedule: the
+// CUs that finish their last gate/up tile go on to down tiles instead of
+// idling through a partly filled last round, and there is no launch between
+// the two.
+//
+// Both tile kinds run the one tile body of the gate/up form (BM rows x two
+// BN-row weight slices): a down tile's two slices are consecutive BN-row
+// blocks of W_d, stored side by side instead of through SwiGLU.
+//
+// A down tile of M-tile m needs every gate/up tile of m.  A gate/up tile
+// writes its h rows with device-scope stores of whole lines (staged through
+// LDS, past its XCD's L2) and is counted in ready[m] once they have completed:
+// at the prologue of the workgroup's next gate/up tile, whose wait drains them
+// anyway, or before the workgroup's first wait and at its end.  A down tile
+// waits until ready[m] holds all of m's gate/up tiles before loading h.  The
+// wait always ends: items are taken in increasing order, so every gate/up
+// tile a down tile waits for was taken earlier by a workgroup that is running
+// it (or holds it as its next item behind a gate/up tile) and waits on
+// nothing.  (The wait also gives up after a bounded number of polls, so the
+// launch drains whatever happens; a give-up is counted in sync[1].)  No h row
+// is read before it is complete, and with rows of whole 128-byte lines (F a
+// multiple of 64, checked by the caller) no line is shared by two M-tiles, so
+// no XCD's L2 can hold a stale copy of an h line (the L2s hold no h lines from
+// earlier launches: each launch starts with them invalidated).
+//
+// sync: [0] the work counter, [1] give-ups, [2 ..] ready[m]; zeroed before the
+// launch (by the index pass).
+constexpr int kReadyPollLimit = 1 << 20;  // about a second of polling
+
+template <int BM, int BN, int WM, int WN, int BK, int NST, int PW, int GM>
+__global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1, 2)))
+void ffn_fused_dma(const bf16* __restrict__ A, const int32_t* __restrict__ gather, int kdiv,
+                   int a_rows, const int32_t* __restrict__ offsets, int E, int rows,
+                   const bf16* __restrict__ wg, const bf16* __restrict__ wu,
+                   const bf16* __restrict__ wd, int d, int F, bf16* __restrict__ h,
+                   bf16* __restrict__ y, int32_t* __restrict__ sync) {
+  // one tile shape for both GEMMs: BM rows x (BN gate + BN up) columns, or
+  // BM rows x 2*BN down columns read as two BN-row slices of W_d (the same
+  // operand loads, LDS layout and MFMA sequence; only the epilogue differs)
+  using C = DmaCfg<BM, BN, WM, WN, true, BK, NST, PW>;
+  __shared__ __align__(1024) unsigned char smem[NST * C::STAGE];
+  __shared__ int s_item[2];  // alternate slots: a slot is rewritten one barrier after it is read
+
+  const int m_tiles = __builtin_amdgcn_readfirstlane(total_mtiles(offsets, E, rows, BM));
+  const int ntg = (F + BN - 1) / BN, ntd = (d + 2 * BN - 1) / (2 * BN);
+  const int n_gu = m_tiles * ntg, n_all = n_gu + m_tiles * ntd;
+  int32_t* ready = sync + 2;
+
+  // The next item is taken from the counter while the current one runs (its
+  // value is needed only at the end), so every item but the first comes
+  // without a wait.  Deadlock-free as without the prefetch: a workgroup
+  // blocked on a down tile holds no unstarted gate/up item, since it took its
+  // prefetched item after its current (down) item and items come in order.
+  if (threadIdx.x == 0) s_item[0] = atomicAdd(&sync[0], 1);
+  lds_barrier();
+  int t = s_item[0];
+  int slot = 0;
+  // M-tile of this workgroup's last gate/up tile, not yet counted in ready[]:
+  // it is counted at the next gate/up tile's prologue (whose wait drains the
+  // stores anyway) or flushed before a wait and at the end
+  int pending = -1;
+  auto flush = [&]() {
+    if (pending >= 0) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (threadIdx.x == 0) atomicAdd(&ready[pending], 1);
+      pending = -1;
+    }
+  };
+  while (t < n_all) {
+    int next = 0;
+    if (threadIdx.x == 0) next = atomicAdd(&sync[0], 1);
+    const bool gu = t < n_gu;
+    int mt, nt, e, row0, row_end;
+    if (gu)
+      tile_coords<GM>(t, ntg, m_tiles, mt, nt);
+    else
+      tile_coords<GM>(t - n_gu, ntd, m_tiles, mt, nt);
+    if (find_tile(offsets, E, rows, BM, mt, e, row0, row_end)) {
+      if (!gu) {
+        flush();
+        if (threadIdx.x == 0) {
+          int polls = 0;
+          while (__hip_atomic_load(&ready[mt], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
+                 ntg) {
+            if (++polls >= kReadyPollLimit) {
+              atomicAdd(&sync[1], 1);
+              break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+          }
+        }
+        __syncthreads();
+      }
+      // h is stored past the XCD's L2 (other XCDs read it in this launch), y
+      // as usual (the next kernel reads it)
+      const GemmArgs g = gu ? GemmArgs{A, gather, kdiv, a_rows, wg, wu, F, d, h,
+                                       (uint32_t)rows * F * 2u, GemmResid{}, false}
+                            : GemmArgs{h, nullptr, 1, rows, wd, nullptr, d, F, y,
+                                       (uint32_t)rows * d * 2u, GemmResid{}, true};
+      gemm_tile<BM, BN, WM, WN, true, BK, NST, PW, false, kScDevice>(
+          smem, g, e, row0, row_end, nt, gu && pending >= 0 ? &ready[pending] : nullptr);
+      if (gu) pending = mt;
+    }
+    // the next item in LDS; this item's LDS use is done everywhere
+    slot ^= 1;
+    if (threadIdx.x == 0) s_item[slot] = next;
+    lds_barrier();
+    t = s_item[slot];
+  }
+  flush();
 }
 
 // Few rows per expert (decode), LDS-staged weight stream.  A workgroup of 4
@@ -1039,6 +1297,25 @@ hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, con
                                       rows, offsets, E, rows, wd, (const bf16*)nullptr, d, F, y, s,
                                       "ffn_down");
   }
+  return hipGetLastError();
+}
+
+size_t ffn_sync_ints(int E, int rows) { return (size_t)ceil_div(rows, 256) + E + 2; }
+
+hipError_t launch_expert_ffn_fused(int E, int d, int F, int rows, const void* A,
+                                   const int32_t* gather, int kdiv, int a_rows,
+                                   const int32_t* offsets, const void* w_gate, const void* w_up,
+                                   const void* w_down, void* y, void* h, int32_t* sync,
+                                   hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  static const int cus = device_cus();
+  ProfileScope ps("ffn_fused", s);
+  FOE_LAUNCH((ffn_fused_dma<256, 128, 2, 4, 64, 2, 4, 4>), dim3(cus),
+             dim3(8 * kWave), 0, s,
+             static_cast<const bf16*>(A), gather, kdiv, a_rows, offsets, E, rows,
+             static_cast<const bf16*>(w_gate), static_cast<const bf16*>(w_up),
+             static_cast<const bf16*>(w_down), d, F, static_cast<bf16*>(h),
+             static_cast<bf16*>(y), sync);
   return hipGetLastError();
 }
 

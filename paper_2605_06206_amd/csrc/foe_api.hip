@@ -9,6 +9,11 @@
 
 #include "foe_common.hpp"
 
+// both grouped GEMMs of the block's expert FFN in one persistent launch
+#ifndef FOE_FFN_FUSED
+#define FOE_FFN_FUSED 1
+#endif
+
 namespace foe {
 namespace {
 
@@ -76,7 +81,7 @@ bool operand_fits(long long rows, long long cols, size_t el) {
 // clusters consecutively (cluster h from h*T*k); one grouped FFN runs over the
 // C*E experts reading x through sorted_src; one kernel combines and reduces.
 struct BlockWs {
-  size_t topk_idx, topk_w, counts, offsets, sorted_src, row_of, y, perm, ffn, cnt, total;
+  size_t topk_idx, topk_w, counts, offsets, sorted_src, row_of, y, perm, ffn, cnt, sync, total;
 };
 
 BlockWs block_ws(foe_dtype dt, int C, int T, int d, int E, int k, int F) {
@@ -98,6 +103,7 @@ BlockWs block_ws(foe_dtype dt, int C, int T, int d, int E, int k, int F) {
   take(w.perm, permute_scratch_bytes(T, k, E, C));
   take(w.ffn, ffn_scratch_bytes(dt, (int)CR, F));
   take(w.cnt, (size_t)T * ceil_div(d, 128) * 4);  // folded-combine arrival counters
+  take(w.sync, ffn_sync_ints(C * E, (int)CR) * 4);  // fused FFN work and ready counters
   w.total = align_up(off, 256);
   return w;
 }
@@ -473,13 +479,26 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
     if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/expert_ffn");
     return FOE_OK;
   }
+  // many rows per expert (bf16): both grouped GEMMs in one persistent launch,
+  // whose counters the index pass clears.  Its h rows must be whole 128-byte
+  // cache lines (F a multiple of 64), so that no line holds rows of two
+  // M-tiles: a down tile then never caches part of a row that another tile is
+  // still writing.
+  const bool fused = FOE_FFN_FUSED && dt == FOE_BF16 && CR >= 64LL * C * E && F % 64 == 0;
+  int32_t* sync = reinterpret_cast<int32_t*>(base + L.sync);
+  const int nsync = fused ? (int)ffn_sync_ints(C * E, (int)CR) : 0;
   // 2. dispatch: expert histogram, prefix sum and stable ranks of all clusters
-  e = launch_index(T, E, k, C, topk_idx, counts, offsets, sorted_src, row_of, perm_ws, s);
+  e = launch_index(T, E, k, C, topk_idx, counts, offsets, sorted_src, row_of, perm_ws, s, sync,
+                   nsync);
   if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/index");
   // 3. one grouped SwiGLU FFN over the C*E experts (weights are [C*E, ...]),
   //    reading the rows of x through sorted_src
-  e = launch_expert_ffn_ex(dt, C * E, d, F, (int)CR, x, sorted_src, k, T, offsets, w_gate, w_up,
-                           w_down, y, ffn_ws, s);
+  if (fused)
+    e = launch_expert_ffn_fused(C * E, d, F, (int)CR, x, sorted_src, k, T, offsets, w_gate, w_up,
+                                w_down, y, ffn_ws, sync, s);
+  else
+    e = launch_expert_ffn_ex(dt, C * E, d, F, (int)CR, x, sorted_src, k, T, offsets, w_gate,
+                             w_up, w_down, y, ffn_ws, s);
   if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/expert_ffn");
   // 4. weighted combine of every cluster and the local cross-cluster reduction
   e = launch_combine_clusters(dt, C, T, d, k, y, row_of, topk_w, x, reduce_scale, out, s);

@@ -105,9 +105,10 @@ int permute_blocks(int R);
 size_t permute_scratch_bytes(int T, int k, int E, int C);
 // histogram / scan / stable ranks of C clusters' ids (topk_idx [C,T,k]);
 // offsets [C*E+1] and row_of values are global rows (cluster h starts at h*T*k)
+// zero [nzero]: int32 counters of the kernel that follows, cleared on the way
 hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int32_t* counts,
                         int32_t* offsets, int32_t* sorted_src, int32_t* row_of, void* scratch,
-                        hipStream_t s);
+                        hipStream_t s, int32_t* zero = nullptr, int nzero = 0);
 hipError_t launch_permute(foe_dtype dt, int T, int d, int E, int k, const int32_t* topk_idx,
                           const void* x, int32_t* counts, int32_t* offsets, int32_t* sorted_src,
                           int32_t* row_of, void* x_perm, void* scratch, hipStream_t s);
@@ -135,6 +136,16 @@ hipError_t launch_group_attention(int H, int S, int d, int nq, int hd, float the
                                   const void* x, const void* w_qkv, const void* w_o, void* r_full,
                                   void* scratch, hipStream_t s);
 
+// bf16 expert FFN with both grouped GEMMs in one persistent launch (many rows
+// per expert): h [rows, F] is its intermediate, sync [ffn_sync_ints(E, rows)]
+// int32 counters that must be zero when it starts.  Operand rows as in
+// launch_expert_ffn_ex.
+size_t ffn_sync_ints(int E, int rows);
+hipError_t launch_expert_ffn_fused(int E, int d, int F, int rows, const void* A,
+                                   const int32_t* gather, int kdiv, int a_rows,
+                                   const int32_t* offsets, const void* w_gate, const void* w_up,
+                                   const void* w_down, void* y, void* h, int32_t* sync,
+                                   hipStream_t s);
 // expert FFN whose operand row r is row gather[r]/kdiv of A (a_rows rows);
 // gather == nullptr: row r of A
 hipError_t launch_expert_ffn_ex(foe_dtype dt, int E, int d, int F, int rows, const void* A,

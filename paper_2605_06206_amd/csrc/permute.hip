@@ -128,7 +128,11 @@ __global__ __launch_bounds__(kChunk) void rank_kernel(
     const int32_t* __restrict__ idx_all, int R, int E, int nbits,
     const int32_t* __restrict__ block_counts_all, const int32_t* __restrict__ block_base_all,
     int32_t* __restrict__ counts_all, int32_t* __restrict__ offsets_all,
-    int32_t* __restrict__ sorted_src_all, int32_t* __restrict__ row_of_all) {
+    int32_t* __restrict__ sorted_src_all, int32_t* __restrict__ row_of_all,
+    int32_t* __restrict__ zero, int nzero) {
+  // counters of the next kernel, cleared on the way (one workgroup)
+  if (blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = threadIdx.x; i < nzero; i += blockDim.x) zero[i] = 0;
   __shared__ int wcnt[kRankWaves][kMaxE];
   __shared__ int total[kMaxE + 1];
   __shared__ int before[kMaxE];
@@ -212,7 +216,11 @@ constexpr int kSmallMaxR = 4096;
 __global__ __launch_bounds__(kSmallWaves * 64) void index_small_kernel(
     const int32_t* __restrict__ idx_all, int R, int E, int nbits,
     int32_t* __restrict__ counts_all, int32_t* __restrict__ offsets_all,
-    int32_t* __restrict__ sorted_src_all, int32_t* __restrict__ row_of_all) {
+    int32_t* __restrict__ sorted_src_all, int32_t* __restrict__ row_of_all,
+    int32_t* __restrict__ zero, int nzero) {
+  // counters of the next kernel, cleared on the way (one workgroup)
+  if (blockIdx.x == 0)
+    for (int i = threadIdx.x; i < nzero; i += blockDim.x) zero[i] = 0;
   const int h = blockIdx.x;
   const int row_base = h * R;
   const int32_t* __restrict__ idx = idx_all + (size_t)h * R;
@@ -331,18 +339,19 @@ hipError_t launch_fill_i32(int32_t* p, int n, int32_t v, hipStream_t s) {
 
 hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int32_t* counts,
                         int32_t* offsets, int32_t* sorted_src, int32_t* row_of, void* scratch,
-                        hipStream_t s) {
+                        hipStream_t s, int32_t* zero, int nzero) {
   const int R = T * k;
   if (R == 0) {
     hipError_t err = launch_fill_i32(offsets, C * E + 1, 0, s);
     if (err == hipSuccess && counts != nullptr) err = launch_fill_i32(counts, C * E, 0, s);
+    if (err == hipSuccess && nzero > 0) err = launch_fill_i32(zero, nzero, 0, s);
     return err;
   }
   const int nbits = E <= 1 ? 0 : 32 - __builtin_clz((unsigned)(E - 1));
   if (R <= kSmallMaxR) {
     ProfileScope ps("permute_index", s);
     FOE_LAUNCH(index_small_kernel, dim3(C), dim3(kSmallWaves * kWave), 0, s, topk_idx, R,
-                       E, nbits, counts, offsets, sorted_src, row_of);
+                       E, nbits, counts, offsets, sorted_src, row_of, zero, nzero);
     return hipGetLastError();
   }
   const int nblk = permute_blocks(R);
@@ -362,10 +371,12 @@ hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int
     ProfileScope ps("permute_rank", s);
     if (fold)
       FOE_LAUNCH(rank_kernel<true>, dim3(nblk, C), dim3(kChunk), 0, s, topk_idx, R, E,
-                         nbits, block_counts, block_base, counts, offsets, sorted_src, row_of);
+                         nbits, block_counts, block_base, counts, offsets, sorted_src, row_of,
+                         zero, nzero);
     else
       FOE_LAUNCH(rank_kernel<false>, dim3(nblk, C), dim3(kChunk), 0, s, topk_idx, R, E,
-                         nbits, block_counts, block_base, counts, offsets, sorted_src, row_of);
+                         nbits, block_counts, block_base, counts, offsets, sorted_src, row_of,
+                         zero, nzero);
   }
   return hipGetLastError();
 }
