@@ -83,7 +83,8 @@ def parse():
 KERNEL_SOURCES = {"route": "route.hip", "permute_index": "permute.hip",
                   "permute_hist": "permute.hip", "permute_rank": "permute.hip",
                   "permute_scan": "permute.hip", "permute_scatter": "permute.hip",
-                  "ffn_gateup": "ffn.hip", "ffn_down": "ffn.hip", "ffn_gateup_f32": "ffn.hip",
+                  "ffn_gateup": "ffn.hip", "ffn_down": "ffn.hip", "ffn_fused": "ffn.hip",
+                  "ffn_gateup_f32": "ffn.hip",
                   "ffn_down_f32": "ffn.hip", "combine": "combine.hip", "reduce": "combine.hip",
                   "attn_qkv": "ffn.hip", "attn_out": "ffn.hip", "attn_prep": "attention.hip",
                   "attn_core": "attention.hip", "attn_xsum": "attention.hip"}
@@ -143,6 +144,11 @@ def kernel_work(name, cfg, e_touched):
         return 4.0 * CR * d * F, 2.0 * e_touched * F * d * s + CR * d * s + CR * F * s
     if name in ("ffn_down", "ffn_down_f32"):
         return 2.0 * CR * F * d, 1.0 * e_touched * d * F * s + CR * F * s + CR * d * s
+    if name == "ffn_fused":
+        # both GEMMs in one launch: the three weight matrices of every touched
+        # expert, the gathered x rows, h written and read back, y written
+        return (6.0 * CR * d * F,
+                3.0 * e_touched * F * d * s + CR * d * s + 2.0 * CR * F * s + CR * d * s)
     if name == "combine":
         # y rows of every cluster, their indices and weights, x, out
         return 2.0 * CR * d, CR * d * s + 8.0 * CR + 2.0 * T * d * s

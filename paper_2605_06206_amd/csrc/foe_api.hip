@@ -81,7 +81,8 @@ bool operand_fits(long long rows, long long cols, size_t el) {
 // clusters consecutively (cluster h from h*T*k); one grouped FFN runs over the
 // C*E experts reading x through sorted_src; one kernel combines and reduces.
 struct BlockWs {
-  size_t topk_idx, topk_w, counts, offsets, sorted_src, row_of, y, perm, ffn, cnt, sync, total;
+  size_t topk_idx, topk_w, counts, offsets, sorted_src, row_of, y, perm, ffn, cnt, sync, rcnt,
+      total;
 };
 
 BlockWs block_ws(foe_dtype dt, int C, int T, int d, int E, int k, int F) {
@@ -104,6 +105,7 @@ BlockWs block_ws(foe_dtype dt, int C, int T, int d, int E, int k, int F) {
   take(w.ffn, ffn_scratch_bytes(dt, (int)CR, F));
   take(w.cnt, (size_t)T * ceil_div(d, 128) * 4);  // folded-combine arrival counters
   take(w.sync, ffn_sync_ints(C * E, (int)CR) * 4);  // fused FFN work and ready counters
+  take(w.rcnt, (size_t)C * ceil_div(T, 16) * E * 4);  // expert counts of the routing blocks
   w.total = align_up(off, 256);
   return w;
 }
@@ -454,11 +456,15 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
   void* ffn_ws = base + L.ffn;
 
   // 1. routing of every cluster in one grid (Section 3.1: one score vector,
-  //    per-group top-k)
+  //    per-group top-k); with many pairs it also counts the experts of its
+  //    token blocks, the histogram of the dispatch
   const bool sel = ffn_sel_ok(dt, C, E, T, k);
+  const RoutePlan rp = plan_route(dt, C, T, d, E, sel);
+  int32_t* rcnt = reinterpret_cast<int32_t*>(base + L.rcnt);
+  const bool use_rc = !sel && index_takes_route_counts(T, E, k, rp.nblk);
   hipError_t e = launch_route(dt, C, T, d, E, k, gating, x, w_router, bias, topk_idx, topk_w, s,
                               sel ? reinterpret_cast<int32_t*>(base + L.cnt) : nullptr,
-                              ceil_div(d, 128));
+                              ceil_div(d, 128), use_rc ? rcnt : nullptr);
   if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/route");
   if (sel) {
     // few pairs per expert: the FFN workgroups list their expert's pairs from
@@ -489,7 +495,7 @@ int foe_cluster_block_ex(foe_dtype dt, int C, int T, int d, int E, int k, int F,
   const int nsync = fused ? (int)ffn_sync_ints(C * E, (int)CR) : 0;
   // 2. dispatch: expert histogram, prefix sum and stable ranks of all clusters
   e = launch_index(T, E, k, C, topk_idx, counts, offsets, sorted_src, row_of, perm_ws, s, sync,
-                   nsync);
+                   nsync, use_rc ? rcnt : nullptr, rp.tok_per_blk, rp.nblk);
   if (e != hipSuccess) return hip_fail(e, "foe_cluster_block/index");
   // 3. one grouped SwiGLU FFN over the C*E experts (weights are [C*E, ...]),
   //    reading the rows of x through sorted_src

@@ -93,10 +93,22 @@ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 // zero_cnt != nullptr: the kernel also clears zero_cnt[T][zero_per_tok].
 // gating: FOE_GATE_RENORM or FOE_GATE_GLOBAL (the global softmax needs every
 // cluster's scores in one workgroup: C == 1 or C*E <= 256).
+// counts != nullptr: the kernel also writes the expert counts of each of its
+// workgroups' tokens, counts [C][nblk][E] (the dispatch histogram; nblk and
+// the tokens per workgroup from plan_route; not with zero_cnt).
+struct RoutePlan {
+  int G = 1;            // clusters scored together in one workgroup
+  bool stream = false;  // the streaming kernel
+  int wpb = 1;          // its waves per workgroup
+  int tok_per_blk = 16; // tokens per workgroup (count block)
+  int nblk = 0;         // workgroups per cluster
+};
+RoutePlan plan_route(foe_dtype dt, int C, int T, int d, int E, bool zero_counters);
 hipError_t launch_route(foe_dtype dt, int C, int T, int d, int E, int k, int gating,
                         const void* x, const void* w_router, const float* bias,
                         int32_t* topk_idx, float* topk_w, hipStream_t s,
-                        int32_t* zero_cnt = nullptr, int zero_per_tok = 0);
+                        int32_t* zero_cnt = nullptr, int zero_per_tok = 0,
+                        int32_t* counts = nullptr);
 // whether all C clusters' scores of a token are formed in one workgroup
 inline bool route_one_pass(int C, int E) { return C == 1 || C * E <= 256; }
 
@@ -105,10 +117,16 @@ int permute_blocks(int R);
 size_t permute_scratch_bytes(int T, int k, int E, int C);
 // histogram / scan / stable ranks of C clusters' ids (topk_idx [C,T,k]);
 // offsets [C*E+1] and row_of values are global rows (cluster h starts at h*T*k)
-// zero [nzero]: int32 counters of the kernel that follows, cleared on the way
+// zero [nzero]: int32 counters of the kernel that follows, cleared on the way.
+// route_counts [C][ncb][E]: expert counts of consecutive blocks of tok_per_cb
+// tokens written by the routing kernel; when index_takes_route_counts() the
+// pass uses them instead of a histogram launch of its own.
+bool index_takes_route_counts(int T, int E, int k, int ncb);
 hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int32_t* counts,
                         int32_t* offsets, int32_t* sorted_src, int32_t* row_of, void* scratch,
-                        hipStream_t s, int32_t* zero = nullptr, int nzero = 0);
+                        hipStream_t s, int32_t* zero = nullptr, int nzero = 0,
+                        const int32_t* route_counts = nullptr, int tok_per_cb = 0,
+                        int ncb = 0);
 hipError_t launch_permute(foe_dtype dt, int T, int d, int E, int k, const int32_t* topk_idx,
                           const void* x, int32_t* counts, int32_t* offsets, int32_t* sorted_src,
                           int32_t* row_of, void* x_perm, void* scratch, hipStream_t s);

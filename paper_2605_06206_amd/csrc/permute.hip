@@ -129,7 +129,7 @@ __global__ __launch_bounds__(kChunk) void rank_kernel(
     const int32_t* __restrict__ block_counts_all, const int32_t* __restrict__ block_base_all,
     int32_t* __restrict__ counts_all, int32_t* __restrict__ offsets_all,
     int32_t* __restrict__ sorted_src_all, int32_t* __restrict__ row_of_all,
-    int32_t* __restrict__ zero, int nzero) {
+    int32_t* __restrict__ zero, int nzero, int ncb, int cb_pairs) {
   // counters of the next kernel, cleared on the way (one workgroup)
   if (blockIdx.x == 0 && blockIdx.y == 0)
     for (int i = threadIdx.x; i < nzero; i += blockDim.x) zero[i] = 0;
@@ -157,20 +157,28 @@ __global__ __launch_bounds__(kChunk) void rank_kernel(
   if (ok && r == 0) wcnt[wave][e] = __popcll(m);
 
   if (FOLD) {
-    // per-expert totals and counts of the earlier blocks, split over
-    // kChunk / E parts of the block list
-    const int32_t* __restrict__ bc = block_counts_all + (size_t)h * nblk * E;
+    // per-expert totals and counts of the pairs before this block, from the
+    // ncb count blocks of cb_pairs pairs each (split over kChunk / E parts of
+    // the count-block list); the pairs of a count block that straddles this
+    // block's start are counted here directly
+    const int32_t* __restrict__ bc = block_counts_all + (size_t)h * ncb * E;
     const int parts = kChunk / E;
     const int pe = tid % E, part = tid / E;
+    const int start = blockIdx.x * kChunk;
+    const int full = start / cb_pairs;  // count blocks wholly before this block
     if (part < parts) {
       int all = 0, bef = 0;
-      for (int b = part; b < nblk; b += parts) {
+      for (int b = part; b < ncb; b += parts) {
         const int c = bc[(size_t)b * E + pe];
         all += c;
-        bef += b < (int)blockIdx.x ? c : 0;
+        bef += b < full ? c : 0;
       }
       atomicAdd(&total[pe], all);
       atomicAdd(&before[pe], bef);
+    }
+    for (int f2 = full * cb_pairs + tid; f2 < start; f2 += kChunk) {
+      const int e2 = idx[f2];
+      if (e2 >= 0 && e2 < E) atomicAdd(&before[e2], 1);
     }
     __syncthreads();
     if (tid < kWave) wave_excl_scan_experts(total, E);
@@ -337,9 +345,15 @@ hipError_t launch_fill_i32(int32_t* p, int n, int32_t v, hipStream_t s) {
   return hipGetLastError();
 }
 
+bool index_takes_route_counts(int T, int E, int k, int ncb) {
+  const long long R = (long long)T * k;
+  return R > kSmallMaxR && (long long)ncb * E <= kFoldMax;
+}
+
 hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int32_t* counts,
                         int32_t* offsets, int32_t* sorted_src, int32_t* row_of, void* scratch,
-                        hipStream_t s, int32_t* zero, int nzero) {
+                        hipStream_t s, int32_t* zero, int nzero, const int32_t* route_counts,
+                        int tok_per_cb, int ncb) {
   const int R = T * k;
   if (R == 0) {
     hipError_t err = launch_fill_i32(offsets, C * E + 1, 0, s);
@@ -355,6 +369,14 @@ hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int
     return hipGetLastError();
   }
   const int nblk = permute_blocks(R);
+  if (route_counts != nullptr && index_takes_route_counts(T, E, k, ncb)) {
+    // the routing kernel counted the experts of its token blocks
+    ProfileScope ps("permute_rank", s);
+    FOE_LAUNCH(rank_kernel<true>, dim3(nblk, C), dim3(kChunk), 0, s, topk_idx, R, E, nbits,
+               route_counts, nullptr, counts, offsets, sorted_src, row_of, zero, nzero, ncb,
+               tok_per_cb * k);
+    return hipGetLastError();
+  }
   int32_t* block_counts = reinterpret_cast<int32_t*>(scratch);
   int32_t* block_base = block_counts + (size_t)C * nblk * E;
   {
@@ -372,11 +394,11 @@ hipError_t launch_index(int T, int E, int k, int C, const int32_t* topk_idx, int
     if (fold)
       FOE_LAUNCH(rank_kernel<true>, dim3(nblk, C), dim3(kChunk), 0, s, topk_idx, R, E,
                          nbits, block_counts, block_base, counts, offsets, sorted_src, row_of,
-                         zero, nzero);
+                         zero, nzero, nblk, kChunk);
     else
       FOE_LAUNCH(rank_kernel<false>, dim3(nblk, C), dim3(kChunk), 0, s, topk_idx, R, E,
                          nbits, block_counts, block_base, counts, offsets, sorted_src, row_of,
-                         zero, nzero);
+                         zero, nzero, nblk, kChunk);
   }
   return hipGetLastError();
 }

@@ -21,6 +21,7 @@ namespace foe {
 namespace {
 
 constexpr int kTok = 16;    // tokens per workgroup
+constexpr int kMaxGE = 256;  // score columns of one routing pass
 #ifndef FOE_ROUTE_BATCH
 #define FOE_ROUTE_BATCH 4
 #endif
@@ -63,6 +64,79 @@ __device__ __forceinline__ void row_softmax_norm(const float (&g)[NT], int col, 
   sm += __int_as_float(row_ror<1>(__float_as_int(sm)));
   m = mx;
   z = sm;
+}
+
+// Top-k of every group and the routing weights of one token whose G*E
+// scores sit in a 16-lane row (column nt*16 + col in g[nt], bias included).
+// sel_e / sel_v: this row's k-slot scratch in LDS (a wave's LDS operations
+// complete in order, so the row reads back what its lane col == 0 wrote).
+// Group h writes topk_*[(h*T + tok)*k + s]; with `hist` (LDS, [G*E]) every
+// selected id is also counted there.
+template <int NT>
+__device__ __forceinline__ void select_token(const float (&g)[NT], int col, int E, int G, int k,
+                                             int gating, int tok, int T_, int* sel_e,
+                                             float* sel_v, int32_t* __restrict__ topk_idx,
+                                             float* __restrict__ topk_w, int* hist) {
+  const int Et = G * E;
+  // global gating: softmax over all G*E scores of the token, not
+  // renormalised over the selection
+  float gm = 0.f, gz = 1.f;
+  if (gating == FOE_GATE_GLOBAL) row_softmax_norm<NT>(g, col, Et, gm, gz);
+  for (int h = 0; h < G; ++h) {
+    // bit nt: column nt*16 + col outside group h or already selected
+    unsigned taken = 0;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int e = nt * 16 + col;
+      if (e < h * E || e >= (h + 1) * E) taken |= 1u << nt;
+    }
+    for (int s = 0; s < k; ++s) {
+      float bv = -__builtin_inff();
+      int be = 0x7fffffff;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int e = nt * 16 + col;
+        if (!((taken >> nt) & 1u) && beats(g[nt], e, bv, be)) { bv = g[nt]; be = e; }
+      }
+      argmax_step<8>(bv, be);
+      argmax_step<4>(bv, be);
+      argmax_step<2>(bv, be);
+      argmax_step<1>(bv, be);
+      if (be != 0x7fffffff && (be & 15) == col) taken |= 1u << (be >> 4);
+      if (col == 0) {
+        sel_e[s] = (be == 0x7fffffff) ? -1 : be - h * E;
+        sel_v[s] = bv;
+      }
+    }
+    // softmax over the selected scores; lane col writes slots col, col+16, ...
+    if (tok < T_) {
+      float m = gm, z = gz;
+      if (gating != FOE_GATE_GLOBAL) {
+        m = sel_v[0];
+        z = 0.f;
+        for (int s = 0; s < k; ++s) z += expf(sel_v[s] - m);
+      }
+      const float inv = 1.0f / z;
+      const size_t o = ((size_t)h * T_ + tok) * k;
+      for (int s = col; s < k; s += 16) {
+        const int id = sel_e[s];
+        topk_idx[o + s] = id;
+        topk_w[o + s] = expf(sel_v[s] - m) * inv;
+        if (hist != nullptr && id >= 0) atomicAdd(&hist[h * E + id], 1);
+      }
+    }
+  }
+}
+
+// Per-workgroup expert counts (the dispatch histogram, folded in): counts
+// [C][gridDim.x][E] of the workgroup's tokens, cluster = blockIdx.y * G + h.
+__device__ __forceinline__ void write_counts(const int* hist, int G, int E,
+                                             int32_t* __restrict__ counts) {
+  for (int i = threadIdx.x; i < G * E; i += blockDim.x) {
+    const int h = i / E, e = i % E;
+    const size_t c = (size_t)blockIdx.y * G + h;
+    counts[(c * gridDim.x + blockIdx.x) * E + e] = hist[i];
+  }
 }
 
 template <typename T> struct RouteMma;
@@ -159,9 +233,16 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
                                                         int d, int E, int k, int G, int gating,
                                                         int32_t* __restrict__ topk_idx,
                                                         float* __restrict__ topk_w,
-                                                        int32_t* __restrict__ zcnt, int zn) {
+                                                        int32_t* __restrict__ zcnt, int zn,
+                                                        int32_t* __restrict__ counts) {
   constexpr int UPW = (4 * TG + NW - 1) / NW;  // units per wave
   extern __shared__ __align__(16) unsigned char smem[];
+  // expert counts (with `counts`): G*E ints after the partial-score and
+  // selection area (the launch sizes the dynamic LDS for both)
+  int* hist = reinterpret_cast<int*>(
+      smem + max((size_t)NW * TG * NT * kWave * sizeof(f32x4), (size_t)NW * 8 * k * 4));
+  if (counts != nullptr)
+    for (int i = threadIdx.x; i < G * E; i += NW * kWave) hist[i] = 0;
   // cluster blockIdx.y: its router matrix, bias and output rows.  With G > 1
   // groups in one workgroup, the G router matrices [G][E][d] are one score
   // matrix of G*E columns and each group's top-k is taken over its own block
@@ -224,77 +305,40 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
     const int unit = wave + u * NW;
     if (unit >= 4 * TG) break;
     const int tok = t0 + (unit >> 2) * 16 + 4 * row + (unit & 3);
-    // global gating: softmax over all G*E scores of the token, not
-    // renormalised over the selection
-    float gm = 0.f, gz = 1.f;
-    if (gating == FOE_GATE_GLOBAL) row_softmax_norm<NT>(gl[u], col, Et, gm, gz);
-    for (int h = 0; h < G; ++h) {
-      // bit nt: column nt*16 + col outside group h or already selected
-      unsigned taken = 0;
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int e = nt * 16 + col;
-        if (e < h * E || e >= (h + 1) * E) taken |= 1u << nt;
-      }
-      for (int s = 0; s < k; ++s) {
-        float bv = -__builtin_inff();
-        int be = 0x7fffffff;
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int e = nt * 16 + col;
-          if (!((taken >> nt) & 1u) && beats(gl[u][nt], e, bv, be)) { bv = gl[u][nt]; be = e; }
-        }
-        argmax_step<8>(bv, be);
-        argmax_step<4>(bv, be);
-        argmax_step<2>(bv, be);
-        argmax_step<1>(bv, be);
-        if (be != 0x7fffffff && (be & 15) == col) taken |= 1u << (be >> 4);
-        if (col == 0) {
-          sel_e[row * k + s] = (be == 0x7fffffff) ? -1 : be - h * E;
-          sel_v[row * k + s] = bv;
-        }
-      }
-      // softmax over the selected scores (this wave's own rows; LDS operations
-      // of one wave complete in order); lane col writes slots col, col+16, ...
-      if (tok < T_) {
-        float m = gm, z = gz;
-        if (gating != FOE_GATE_GLOBAL) {
-          m = sel_v[row * k];
-          z = 0.f;
-          for (int s = 0; s < k; ++s) z += expf(sel_v[row * k + s] - m);
-        }
-        const float inv = 1.0f / z;
-        const size_t o = ((size_t)h * T_ + tok) * k;
-        for (int s = col; s < k; s += 16) {
-          topk_idx[o + s] = sel_e[row * k + s];
-          topk_w[o + s] = expf(sel_v[row * k + s] - m) * inv;
-        }
-      }
-    }
+    select_token<NT>(gl[u], col, E, G, k, gating, tok, T_, sel_e + row * k, sel_v + row * k,
+                     topk_idx, topk_w, counts != nullptr ? hist : nullptr);
+  }
+  if (counts != nullptr) {
+    __syncthreads();
+    write_counts(hist, G, E, counts);
   }
 }
 
-// Many tokens, bf16, E <= 32: a workgroup of WPB waves takes 16 tokens per
-// wave over all of K, so no partial scores are exchanged.  x and W_r stream
-// through a ring of NS LDS stages of 128 K columns with LDS-DMA loads of 4
-// rows x 256 bytes (each wave loads its own token rows and a share of the
-// router rows), the 16-byte chunk c of row r stored in slot c ^ (r & 15).
-// Each wave then selects the top-k of its tokens from its own accumulators.
+// Many tokens, bf16, G*E <= 64: a workgroup of WPB waves takes 16 tokens per
+// wave over all of K, so no partial scores are exchanged.  x and the G*E
+// router rows stream through a ring of NS LDS stages of 128 K columns with
+// LDS-DMA loads of 4 rows x 256 bytes (each wave loads its own token rows and
+// a share of the router rows, which all waves of the workgroup use), the
+// 16-byte chunk c of row r stored in slot c ^ (r & 15).  Each wave then
+// selects every group's top-k of its tokens from its own accumulators.
 template <int NT, int NS, int WPB>
 __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
     const bf16* __restrict__ x, const bf16* __restrict__ w, const float* __restrict__ bias,
-    int T_, int d, int E, int k, int gating, int32_t* __restrict__ topk_idx,
-    float* __restrict__ topk_w) {
+    int T_, int d, int E, int G, int k, int gating, int32_t* __restrict__ topk_idx,
+    float* __restrict__ topk_w, int32_t* __restrict__ counts) {
   constexpr int XB = WPB * 4096;          // token rows of a stage (16 rows x 256 B per wave)
-  constexpr int SB = XB + NT * 4096;      // + router rows (16 rows x 256 B per expert tile)
-  constexpr int WI = NT * 4 / WPB;        // router instructions per wave and stage
+  constexpr int SB = XB + NT * 4096;      // + router rows (16 rows x 256 B per score tile)
+  constexpr int WI = NT * 4 / WPB;        // router DMA instructions per wave and stage
   constexpr int NI = 4 + WI;              // DMA instructions per wave and stage
   static_assert(NT * 4 % WPB == 0, "even split of the router rows");
-  static_assert(NS * SB + WPB * 8 * 32 * 4 <= 160 * 1024, "LDS capacity");
+  static_assert(NS * SB + WPB * 8 * 64 * 4 + kMaxGE * 4 <= 160 * 1024, "LDS capacity");
   __shared__ __align__(1024) unsigned char smem[NS * SB];
-  __shared__ int sel_buf[WPB][8 * 32];
+  __shared__ int sel_buf[WPB][8 * 64];  // per row of 16 lanes: k ids, k scores (k <= 64)
+  __shared__ int hist[kMaxGE];
+  const int Et = G * E;  // score columns
+  for (int i = threadIdx.x; i < Et; i += WPB * kWave) hist[i] = 0;
 
-  // cluster blockIdx.y: its router matrix, bias and output rows
+  // cluster blockIdx.y (G == 1): its router matrix, bias and output rows
   w += (size_t)blockIdx.y * E * d;
   if (bias != nullptr) bias += (size_t)blockIdx.y * E;
   topk_idx += (size_t)blockIdx.y * T_ * k;
@@ -304,7 +348,7 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
   const int t0 = (blockIdx.x * WPB + wave) * 16;  // this wave's tokens
   const uint32_t lds0 = lds_addr(smem);
   const __amdgpu_buffer_rsrc_t xr = make_rsrc_u(x, (uint32_t)T_ * d * 2u);
-  const __amdgpu_buffer_rsrc_t wr = make_rsrc_u(w, (uint32_t)E * d * 2u);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc_u(w, (uint32_t)Et * d * 2u);
   const int lr = lane >> 4, lc = lane & 15;
   // token instruction i (rows t0+4i..) and router instruction wave*WI + j
   uint32_t xv[4], wv[WI];
@@ -321,7 +365,7 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
     const int e = 4 * (wave * WI + j) + lr;  // router row
     const int q = lc ^ (e & 15);
     wk[j] = q * 8;
-    wv[j] = e < E ? ((uint32_t)e * d + q * 8) * 2u : kOob;
+    wv[j] = e < Et ? ((uint32_t)e * d + q * 8) * 2u : kOob;
   }
   const int nks = (d + 127) / 128;
   auto issue = [&](int kt, int s) {
@@ -371,56 +415,24 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
   }
 
   // accumulator register i holds token t0 + 4*(lane/16) + i (one per 16-lane
-  // row) and experts nt*16 + lane%16
+  // row) and score columns nt*16 + lane%16
   const int col = lane & 15, row = lane >> 4;
-  int* sel_e = sel_buf[wave];
-  float* sel_v = reinterpret_cast<float*>(sel_e + 4 * k);
+  int* sel_e = sel_buf[wave] + row * 2 * k;
+  float* sel_v = reinterpret_cast<float*>(sel_e + k);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     float gl[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int e = nt * 16 + col;
-      gl[nt] = acc[nt][i] + ((bias != nullptr && e < E) ? bias[e] : 0.f);
+      gl[nt] = acc[nt][i] + ((bias != nullptr && e < Et) ? bias[e] : 0.f);
     }
-    const int tok = t0 + 4 * row + i;
-    float gm = 0.f, gz = 1.f;  // global gating: softmax over all E scores
-    if (gating == FOE_GATE_GLOBAL) row_softmax_norm<NT>(gl, col, E, gm, gz);
-    unsigned taken = 0;  // bit nt: expert nt*16 + col already selected / absent
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      if (nt * 16 + col >= E) taken |= 1u << nt;
-    for (int s = 0; s < k; ++s) {
-      float bv = -__builtin_inff();
-      int be = 0x7fffffff;
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int e = nt * 16 + col;
-        if (!((taken >> nt) & 1u) && beats(gl[nt], e, bv, be)) { bv = gl[nt]; be = e; }
-      }
-      argmax_step<8>(bv, be);
-      argmax_step<4>(bv, be);
-      argmax_step<2>(bv, be);
-      argmax_step<1>(bv, be);
-      if (be != 0x7fffffff && (be & 15) == col) taken |= 1u << (be >> 4);
-      if (col == 0) {
-        sel_e[row * k + s] = (be == 0x7fffffff) ? -1 : be;
-        sel_v[row * k + s] = bv;
-      }
-    }
-    if (tok < T_) {
-      float m = gm, z = gz;
-      if (gating != FOE_GATE_GLOBAL) {
-        m = sel_v[row * k];
-        z = 0.f;
-        for (int s = 0; s < k; ++s) z += expf(sel_v[row * k + s] - m);
-      }
-      const float inv = 1.0f / z;
-      for (int s = col; s < k; s += 16) {
-        topk_idx[(size_t)tok * k + s] = sel_e[row * k + s];
-        topk_w[(size_t)tok * k + s] = expf(sel_v[row * k + s] - m) * inv;
-      }
-    }
+    select_token<NT>(gl, col, E, G, k, gating, t0 + 4 * row + i, T_, sel_e, sel_v, topk_idx,
+                     topk_w, counts != nullptr ? hist : nullptr);
+  }
+  if (counts != nullptr) {
+    __syncthreads();
+    write_counts(hist, G, E, counts);
   }
 }
 
@@ -428,15 +440,15 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
 template <typename T, int NT, int NW, int TG, int KB = kBatch>
 hipError_t launch_nt(int C, int G, int T_, int d, int E, int k, int gating, const void* x,
                      const void* w, const float* bias, int32_t* idx, float* wt, hipStream_t s,
-                     int32_t* zcnt, int zn) {
+                     int32_t* zcnt, int zn, int32_t* counts) {
   size_t lds_red = (size_t)NW * TG * NT * kWave * sizeof(f32x4);
   size_t lds_sel = (size_t)NW * 8 * k * 4;
-  size_t lds = lds_red > lds_sel ? lds_red : lds_sel;
+  size_t lds = (lds_red > lds_sel ? lds_red : lds_sel) + (counts != nullptr ? G * E * 4 : 0);
   dim3 grid(ceil_div(T_, kTok * TG), C / G);
   ProfileScope ps("route", s);
   FOE_LAUNCH((route_kernel<T, NT, NW, TG, KB>), grid, dim3(NW * kWave), lds, s,
              reinterpret_cast<const T*>(x), reinterpret_cast<const T*>(w), bias, T_, d, E, k, G,
-             gating, idx, wt, zcnt, zn);
+             gating, idx, wt, zcnt, zn, counts);
   return hipGetLastError();
 }
 
@@ -450,8 +462,23 @@ template <int TG_, int NW_> struct RouteCfg {
 #ifndef FOE_ROUTE_STREAM
 #define FOE_ROUTE_STREAM 1
 #endif
+// streaming kernel from this many tokens (two 16-token waves per CU or more)
 #ifndef FOE_ROUTE_STREAM_MIN_T
 #define FOE_ROUTE_STREAM_MIN_T 8192
+#endif
+// streaming kernel: waves per workgroup by token count (>= 16384, >= 8192,
+// fewer) and LDS ring stages
+#ifndef FOE_ROUTE_WPB_L
+#define FOE_ROUTE_WPB_L 4
+#endif
+#ifndef FOE_ROUTE_WPB_M
+#define FOE_ROUTE_WPB_M 2
+#endif
+#ifndef FOE_ROUTE_WPB_S
+#define FOE_ROUTE_WPB_S 1
+#endif
+#ifndef FOE_ROUTE_NS
+#define FOE_ROUTE_NS 4
 #endif
 #ifndef FOE_ROUTE_SMALL_NW
 #define FOE_ROUTE_SMALL_NW 8
@@ -465,76 +492,106 @@ template <int TG_, int NW_> struct RouteCfg {
 #ifndef FOE_ROUTE_TG64
 #define FOE_ROUTE_TG64 1, 8
 #endif
-template <int WPB>
-hipError_t launch_stream(int C, int T_, int d, int E, int k, int gating, const void* x,
-                         const void* w, const float* bias, int32_t* idx, float* wt,
-                         hipStream_t s) {
-  constexpr int NS = 4;
-  dim3 grid(ceil_div(T_, 16 * WPB), C);
-  const bf16* xb = reinterpret_cast<const bf16*>(x);
-  const bf16* wb = reinterpret_cast<const bf16*>(w);
-  if (E <= 16)
-    FOE_LAUNCH((route_stream_kernel<1, NS, WPB>), grid, dim3(WPB * kWave), 0, s, xb, wb,
-                       bias, T_, d, E, k, gating, idx, wt);
-  else
-    FOE_LAUNCH((route_stream_kernel<2, NS, WPB>), grid, dim3(WPB * kWave), 0, s, xb, wb,
-                       bias, T_, d, E, k, gating, idx, wt);
+
+template <int NT, int WPB>
+hipError_t launch_stream_nt(int C, int G, int T_, int d, int E, int k, int gating, const void* x,
+                            const void* w, const float* bias, int32_t* idx, float* wt,
+                            int32_t* counts, hipStream_t s) {
+  dim3 grid(ceil_div(T_, 16 * WPB), C / G);
+  FOE_LAUNCH((route_stream_kernel<NT, FOE_ROUTE_NS, WPB>), grid, dim3(WPB * kWave), 0, s,
+             reinterpret_cast<const bf16*>(x), reinterpret_cast<const bf16*>(w), bias, T_, d,
+             E, G, k, gating, idx, wt, counts);
   return hipGetLastError();
 }
 
+template <int WPB>
+hipError_t launch_stream(int C, int G, int T_, int d, int E, int k, int gating, const void* x,
+                         const void* w, const float* bias, int32_t* idx, float* wt,
+                         int32_t* counts, hipStream_t s) {
+  ProfileScope ps("route", s);
+  const int Et = G * E;
+  if (Et <= 16)
+    return launch_stream_nt<1, WPB>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, counts, s);
+  if (Et <= 32)
+    return launch_stream_nt<2, WPB>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, counts, s);
+  return launch_stream_nt<4, WPB>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, counts, s);
+}
+
 template <typename T>
-hipError_t launch_t(int C, int T_, int d, int E, int k, int gating, const void* x, const void* w,
-                    const float* bias, int32_t* idx, float* wt, hipStream_t s, int32_t* zcnt,
-                    int zn) {
-  const bool many = T_ >= 2048;
-  // several clusters: one pass over x scores all C*E experts (the router
-  // matrices are contiguous) and each cluster takes its top-k from its block
-  const int G = (C > 1 && C * E <= 256) ? C : 1;
+hipError_t launch_t(const RoutePlan& p, int C, int T_, int d, int E, int k, int gating,
+                    const void* x, const void* w, const float* bias, int32_t* idx, float* wt,
+                    hipStream_t s, int32_t* zcnt, int zn, int32_t* counts) {
+  const int G = p.G;
   const int Et = G * E;
   if constexpr (sizeof(T) == 2) {
-    // buffer offsets are 32-bit: x must span less than 2 GiB
-    if (FOE_ROUTE_STREAM && G == 1 && zcnt == nullptr && T_ >= FOE_ROUTE_STREAM_MIN_T &&
-        E <= 32 && (size_t)T_ * d * 2 < ((size_t)1 << 31)) {
-      // more waves per workgroup share each router row once there are enough
-      // tokens for every CU
-      ProfileScope ps("route", s);
-      if (T_ >= 16384)
-        return launch_stream<4>(C, T_, d, E, k, gating, x, w, bias, idx, wt, s);
-      return launch_stream<2>(C, T_, d, E, k, gating, x, w, bias, idx, wt, s);
+    if (p.stream) {
+      if (p.wpb == 4)
+        return launch_stream<4>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, counts, s);
+      if (p.wpb == 2)
+        return launch_stream<2>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, counts, s);
+      return launch_stream<1>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, counts, s);
     }
   }
+  const bool many = T_ >= 2048;
   if (Et <= 16)
     return many ? launch_nt<T, 1, RouteCfg<FOE_ROUTE_TG16>::NW, RouteCfg<FOE_ROUTE_TG16>::TG>(
-                      C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn)
+                      C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn, counts)
                 : launch_nt<T, 1, FOE_ROUTE_SMALL_NW, 1>(C, G, T_, d, E, k, gating, x, w, bias,
-                                                          idx, wt, s, zcnt, zn);
+                                                          idx, wt, s, zcnt, zn, counts);
   if (Et <= 32)
     return many ? launch_nt<T, 2, RouteCfg<FOE_ROUTE_TG32>::NW, RouteCfg<FOE_ROUTE_TG32>::TG>(
-                      C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn)
+                      C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn, counts)
                 : launch_nt<T, 2, FOE_ROUTE_SMALL_NW, 1>(C, G, T_, d, E, k, gating, x, w, bias,
-                                                          idx, wt, s, zcnt, zn);
+                                                          idx, wt, s, zcnt, zn, counts);
   if (Et <= 64)
     return many ? launch_nt<T, 4, RouteCfg<FOE_ROUTE_TG64>::NW, RouteCfg<FOE_ROUTE_TG64>::TG>(
-                      C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn)
+                      C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn, counts)
                 : launch_nt<T, 4, 8, 1>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt,
-                                        zn);
+                                        zn, counts);
   if (Et <= 128)
-    return launch_nt<T, 8, 4, 1>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn);
-  return launch_nt<T, 16, 4, 1>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn);
+    return launch_nt<T, 8, 4, 1>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn,
+                                 counts);
+  return launch_nt<T, 16, 4, 1>(C, G, T_, d, E, k, gating, x, w, bias, idx, wt, s, zcnt, zn,
+                                counts);
 }
 
 }  // namespace
 
+RoutePlan plan_route(foe_dtype dt, int C, int T, int d, int E, bool zero_counters) {
+  RoutePlan p;
+  // several clusters: one pass over x scores all C*E experts (the router
+  // matrices are contiguous) and each cluster takes its top-k from its block
+  p.G = (C > 1 && C * E <= 256) ? C : 1;
+  const int Et = p.G * E;
+  // buffer offsets are 32-bit: x must span less than 2 GiB
+  p.stream = FOE_ROUTE_STREAM && dt == FOE_BF16 && !zero_counters &&
+             T >= FOE_ROUTE_STREAM_MIN_T && Et <= 64 && (size_t)T * d * 2 < ((size_t)1 << 31);
+  p.wpb = T >= 16384 ? FOE_ROUTE_WPB_L : T >= 8192 ? FOE_ROUTE_WPB_M : FOE_ROUTE_WPB_S;
+  if (p.stream) {
+    p.tok_per_blk = 16 * p.wpb;
+  } else {
+    const bool many = T >= 2048;
+    int tg = 1;
+    if (many && Et <= 16) tg = RouteCfg<FOE_ROUTE_TG16>::TG;
+    else if (many && Et <= 32) tg = RouteCfg<FOE_ROUTE_TG32>::TG;
+    else if (many && Et <= 64) tg = RouteCfg<FOE_ROUTE_TG64>::TG;
+    p.tok_per_blk = kTok * tg;
+  }
+  p.nblk = ceil_div(T, p.tok_per_blk);
+  return p;
+}
+
 hipError_t launch_route(foe_dtype dt, int C, int T, int d, int E, int k, int gating,
                         const void* x, const void* w_router, const float* bias,
                         int32_t* topk_idx, float* topk_w, hipStream_t s, int32_t* zero_cnt,
-                        int zero_per_tok) {
+                        int zero_per_tok, int32_t* counts) {
   if (T == 0 || C == 0) return hipSuccess;
+  const RoutePlan p = plan_route(dt, C, T, d, E, zero_cnt != nullptr);
   if (dt == FOE_BF16)
-    return launch_t<bf16>(C, T, d, E, k, gating, x, w_router, bias, topk_idx, topk_w, s,
-                          zero_cnt, zero_per_tok);
-  return launch_t<float>(C, T, d, E, k, gating, x, w_router, bias, topk_idx, topk_w, s,
-                         zero_cnt, zero_per_tok);
+    return launch_t<bf16>(p, C, T, d, E, k, gating, x, w_router, bias, topk_idx, topk_w, s,
+                          zero_cnt, zero_per_tok, counts);
+  return launch_t<float>(p, C, T, d, E, k, gating, x, w_router, bias, topk_idx, topk_w, s,
+                         zero_cnt, zero_per_tok, counts);
 }
 
 }  // namespace foe

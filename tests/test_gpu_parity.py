@@ -172,6 +172,33 @@ def test_route_global_gating(G, T, d, E, k, dt):
         assert np.max(np.abs(total - 1.0)) <= 1e-5
 
 
+@pytest.mark.parametrize("G,T,d,E,k,gating", [
+    (8, 4096, 2048, 8, 2, "renorm"),    # the layer-share shape: 64 score columns, one pass
+    (3, 4100, 136, 20, 3, "renorm"),    # ragged tokens and K, groups straddle score tiles
+    (2, 9000, 264, 16, 4, "global"),    # two waves per workgroup
+    (4, 16400, 128, 16, 2, "renorm"),   # four waves per workgroup, ragged last block
+    (5, 4096, 64, 12, 12, "renorm"),    # k = E inside every group
+])
+def test_route_grouped_streaming(G, T, d, E, k, gating):
+    """Several clusters scored in one pass over x by the streaming kernel
+    (G*E <= 64 score columns, T >= 4096), each taking its top-k over its own
+    block of E columns."""
+    say("route grouped streaming", G, T, d, E, k, gating)
+    rng = np.random.default_rng([G, T, E])
+    xs = synth.round_to_bf16(rng.standard_normal((T, d)).astype(np.float32))
+    wr = synth.round_to_bf16((rng.standard_normal((G, E, d)) * 0.05).astype(np.float32))
+    bias = (rng.standard_normal((G, E)) * 0.1).astype(np.float32)
+    gidx, gw = foe.route(to_dev(xs, "bf16"), to_dev(wr, "bf16"), to_dev(bias, "f32"), k,
+                         gating=gating)
+    gidx, gw = host(gidx).reshape(G, T, k), host(gw).reshape(G, T, k)
+    refs = [oracle.route(xs, wr[h], bias[h], k) for h in range(G)]
+    if gating == "global":
+        ws = oracle.gate_weights_global([r["logits"] for r in refs], [r["idx"] for r in refs])
+        refs = [dict(r, w=w) for r, w in zip(refs, ws)]
+    for h in range(G):
+        check_route(gidx[h], gw[h], refs[h], TOL["bf16"], sums_to_one=gating == "renorm")
+
+
 @pytest.mark.parametrize("k", [1, 3])
 def test_route_exact_ties_pick_lower_id(k):
     """Duplicate router rows give bit-identical scores on both sides: the
@@ -417,6 +444,8 @@ def test_block_parity_large_configs(name):
     (5000, 64, 8, 2, 64, 2, None, "bf16", None),      # two clusters, multi-block dispatch
     (40, 136, 6, 2, 200, 2, None, "bf16", None),      # decode form, d and F off the tile widths
     (70, 64, 10, 3, 64, 3, None, "bf16", "zipf1.2"),  # cluster blocks straddle 16-column tiles
+    (4500, 64, 10, 3, 128, 2, None, "bf16", None),    # routing counts in 48-pair blocks
+    (8300, 72, 16, 2, 64, 1, None, "bf16", "zipf1.2"),  # two-wave routing blocks, ragged
 ])
 def test_block_parity_shapes(T, d, E, k, F, C, scale, dt, bias):
     say("block shapes", T, d, E, k, F, C, scale, dt, bias)
