@@ -702,8 +702,9 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
 
 // Both grouped GEMMs of the expert FFN in one persistent launch.  Work items
 // are the gate/up tiles (SwiGLU epilogue, writing h) followed by the down
-// tiles (reading h, writing y), numbered in that order and handed out one at a
-// time from a device-side counter, so the two GEMMs share one schedule: the
+// tiles (reading h, writing y), numbered in that order; a workgroup's first
+// item is its own index and the later ones come one at a time, in order, from
+// a device-side counter, so the two GEMMs share one schedule: the
 // CUs that finish their last gate/up tile go on to down tiles instead of
 // idling through a partly filled last round, and there is no launch between
 // the two.
@@ -718,10 +719,10 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
 // at the prologue of the workgroup's next gate/up tile, whose wait drains them
 // anyway, or before the workgroup's first wait and at its end.  A down tile
 // waits until ready[m] holds all of m's gate/up tiles before loading h.  The
-// wait always ends: items are taken in increasing order, so every gate/up
-// tile a down tile waits for was taken earlier by a workgroup that is running
-// it (or holds it as its next item behind a gate/up tile) and waits on
-// nothing.  (The wait also gives up after a bounded number of polls, so the
+// wait always ends: every gate/up tile a down tile waits for is the first
+// item of a workgroup of the grid or was taken from the counter, in order,
+// before the down tile, by a workgroup that is running it (or holds it as its
+// next item behind a gate/up tile); gate/up tiles wait on nothing.  (The wait also gives up after a bounded number of polls, so the
 // launch drains whatever happens; a give-up is counted in sync[1].)  No h row
 // is read before it is complete, and with rows of whole 128-byte lines (F a
 // multiple of 64, checked by the caller) no line is shared by two M-tiles, so
@@ -753,12 +754,14 @@ void ffn_fused_dma(const bf16* __restrict__ A, const int32_t* __restrict__ gathe
 
   // The next item is taken from the counter while the current one runs (its
   // value is needed only at the end), so every item but the first comes
-  // without a wait.  Deadlock-free as without the prefetch: a workgroup
-  // blocked on a down tile holds no unstarted gate/up item, since it took its
-  // prefetched item after its current (down) item and items come in order.
-  if (threadIdx.x == 0) s_item[0] = atomicAdd(&sync[0], 1);
-  lds_barrier();
-  int t = s_item[0];
+  // without a wait.  Deadlock-free: a workgroup blocked on a down tile holds
+  // no unstarted gate/up item (its next item was taken after its current,
+  // down, item, and items come in order), and the gate/up items that are
+  // first items belong to workgroups of the grid, which run to their end.
+  // the first item of every workgroup is its own index (a workgroup that
+  // starts early cannot take two first-round items); later ones come from the
+  // counter, numbered after the grid
+  int t = blockIdx.x;
   int slot = 0;
   // M-tile of this workgroup's last gate/up tile, not yet counted in ready[]:
   // it is counted at the next gate/up tile's prologue (whose wait drains the
@@ -774,7 +777,7 @@ void ffn_fused_dma(const bf16* __restrict__ A, const int32_t* __restrict__ gathe
   };
   while (t < n_all) {
     int next = 0;
-    if (threadIdx.x == 0) next = atomicAdd(&sync[0], 1);
+    if (threadIdx.x == 0) next = (int)gridDim.x + atomicAdd(&sync[0], 1);
     const bool gu = t < n_gu;
     int mt, nt, e, row0, row_end;
     if (gu)
