@@ -503,8 +503,17 @@ def prepare_block(args, name):
     def timed(n_steps, run):
         return timed_on(stream, n_steps, run)
 
-    return lambda: measure_block(args, name, cfg, foe, stream, nsets, sets, calls, out, step,
-                                 timed, e_touched)
+    # the closure holds every buffer the raw pointers in `calls` point into
+    # (inputs, workspace, output) until the workload has been measured
+    keep = {"sets": sets, "ws": ws, "out": out}
+
+    def run_measure():
+        rec = measure_block(args, name, cfg, foe, stream, nsets, sets, calls, out, step, timed,
+                            e_touched)
+        keep.clear()
+        return rec
+
+    return run_measure
 
 
 def measure_block(args, name, cfg, foe, stream, nsets, sets, calls, out, step, timed, e_touched):

@@ -446,6 +446,8 @@ def test_block_parity_large_configs(name):
     (70, 64, 10, 3, 64, 3, None, "bf16", "zipf1.2"),  # cluster blocks straddle 16-column tiles
     (4500, 64, 10, 3, 128, 2, None, "bf16", None),    # routing counts in 48-pair blocks
     (8300, 72, 16, 2, 64, 1, None, "bf16", "zipf1.2"),  # two-wave routing blocks, ragged
+    (40000, 64, 4, 2, 64, 1, None, "bf16", None),     # 79 tile groups: per-XCD work lists
+    (30000, 128, 6, 2, 128, 2, None, "bf16", "zipf1.2"),  # per-XCD lists, two clusters, skew
 ])
 def test_block_parity_shapes(T, d, E, k, F, C, scale, dt, bias):
     say("block shapes", T, d, E, k, F, C, scale, dt, bias)
