@@ -55,6 +55,13 @@ __device__ __forceinline__ u32x4 zero_u32x4() { return u32x4{0u, 0u, 0u, 0u}; }
 // ---- wave helpers ----------------------------------------------------------
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
+// v unchanged, through an empty volatile asm: the compiler cannot move values
+// derived from the result above this point (e.g. hoist them out of a loop).
+__device__ __forceinline__ int opaque_int(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 // Rotate a 32-bit value right by `sh` lanes inside each row of 16 lanes (DPP).
 template <int SH>
 __device__ __forceinline__ int row_ror(int v) {
