@@ -536,26 +536,39 @@ __device__ __forceinline__ void gemm_tile(unsigned char* smem, const GemmArgs& g
 
     // K steps rounded up to a multiple of NST: steps past K read zeros.
     // The DMA of stage kt+NST-1 is spread over the k16 steps of iteration kt:
-    // with two stages it must be complete at this iteration's barrier, so it
-    // goes out in the first KS-2 steps (at least one); with more stages it may
-    // use every step.  DS = steps carrying DMA, Q(s) = first instruction of
-    // step s, BEFORE = instructions issued before the barrier.
+    // with more than two stages it may use every step.  With two stages it
+    // must be complete at this iteration's barrier, and (EARLY) its first QE
+    // instructions already go out in the last k16 step of iteration kt-1:
+    // that step follows the barrier after which no wave reads the buffer of
+    // stage kt-1 any more, so the loads of a stage start one k16 step sooner
+    // and have about half as long again to arrive (the stage waits at the
+    // barrier were most of what separated the loop from the MFMA rate).
+    // DS = steps carrying the rest, Q(s) = first instruction of step s,
+    // BEFORE = instructions issued before the barrier.
     const int nk = ((K + BK - 1) / BK + NST - 1) / NST * NST;
     constexpr int KS = C::KS;
-    constexpr int DS = NST == 2 ? (KS - 2 > 1 ? KS - 2 : 1) : KS;
+    constexpr bool EARLY = NST == 2 && KS >= 3;
+#ifndef FOE_DMA_EARLY_Q  // eighths of a stage's instructions issued early
+#define FOE_DMA_EARLY_Q 4
+#endif
+    constexpr int QE = EARLY ? NLD * FOE_DMA_EARLY_Q / 8 : 0;
+    constexpr int DS = EARLY ? 1 : (NST == 2 ? (KS - 2 > 1 ? KS - 2 : 1) : KS);
     constexpr int BEFORE = NST == 2 ? NLD : (KS - 1) * NLD / KS;
     // loads allowed in flight at the barrier of iteration kt (stage kt+1
     // complete): the later stages' DMAs issued so far
     constexpr int VM_AT_BARRIER = NST == 2 ? 0 : (NST - 3) * NLD + BEFORE;
     static_assert(VM_AT_BARRIER <= 63, "vmcnt range");
-    auto qof = [&](int st) { return st >= DS ? NLD : st * NLD / DS; };
+    auto qof = [&](int st) { return st >= DS ? NLD : QE + st * (NLD - QE) / DS; };
     auto iteration = [&](auto producer, int kt, int b) {
       const int dkt = kt + NST - 1, dbuf = (b + NST - 1) % NST;
 #pragma unroll
       for (int st = 0; st + 1 < KS; ++st)
         kstep(producer, st & 1, b, st + 1, dkt, dbuf, qof(st), qof(st + 1));
       vm_barrier<VM_AT_BARRIER>();
-      kstep(producer, (KS - 1) & 1, (b + 1) % NST, 0, dkt, dbuf, qof(KS - 1), qof(KS));
+      if constexpr (EARLY)  // stage kt+2 into the buffer of stage kt
+        kstep(producer, (KS - 1) & 1, (b + 1) % NST, 0, kt + 2, b, 0, QE);
+      else
+        kstep(producer, (KS - 1) & 1, (b + 1) % NST, 0, dkt, dbuf, qof(KS - 1), qof(KS));
     };
     // the K loop, specialised for issuing and non-issuing waves (both meet
     // the same barriers)
@@ -565,13 +578,17 @@ __device__ __forceinline__ void gemm_tile(unsigned char* smem, const GemmArgs& g
         for (int st = 0; st < NST - 1; ++st)
 #pragma unroll
           for (int q = 0; q < NLD; ++q) issue_one(st, st, q);
+        if constexpr (EARLY) {  // the early part of stage 1
+#pragma unroll
+          for (int q = 0; q < QE; ++q) issue_one(1, 1, q);
+        }
       }
-      vm_barrier<NLD * (NST - 2)>();
+      vm_barrier<EARLY ? QE : NLD * (NST - 2)>();
       // `signal`: counted once every wave's earlier stores have completed
-      // (with two stages the wait above drains every earlier memory
-      // operation of the wave, and the barrier meets all waves)
+      // (the wait drains every earlier memory operation of the wave, and the
+      // barrier meets all waves)
       if (signal != nullptr) {
-        if constexpr (NST != 2) vm_barrier<0>();
+        if constexpr (NST != 2 || EARLY) vm_barrier<0>();
         if (threadIdx.x == 0) atomicAdd(signal, 1);
       }
       fload(0, 0, 0);
