@@ -331,6 +331,7 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
   constexpr int WI = NT * 4 / WPB;        // router DMA instructions per wave and stage
   constexpr int NI = 4 + WI;              // DMA instructions per wave and stage
   static_assert(NT * 4 % WPB == 0, "even split of the router rows");
+  static_assert(NS >= 2 && NI * (NS - 2) <= 63, "vmcnt range");
   static_assert(NS * SB + WPB * 8 * 64 * 4 + kMaxGE * 4 <= 160 * 1024, "LDS capacity");
   __shared__ __align__(1024) unsigned char smem[NS * SB];
   __shared__ int sel_buf[WPB][8 * 64];  // per row of 16 lanes: k ids, k scores (k <= 64)
@@ -497,8 +498,15 @@ template <int NT, int WPB>
 hipError_t launch_stream_nt(int C, int G, int T_, int d, int E, int k, int gating, const void* x,
                             const void* w, const float* bias, int32_t* idx, float* wt,
                             int32_t* counts, hipStream_t s) {
+  // as many ring stages as the LDS holds, up to FOE_ROUTE_NS
+  // (and as the vmcnt field can count: NI * (NS - 2) <= 63 loads in flight)
+  constexpr int SB = (WPB + NT) * 4096;
+  constexpr int NI = 4 + NT * 4 / WPB;
+  constexpr int NS_FIT = (150 * 1024) / SB, NS_VM = 2 + 63 / NI;
+  constexpr int NS_MAX = NS_FIT < NS_VM ? NS_FIT : NS_VM;
+  constexpr int NS = NS_MAX < FOE_ROUTE_NS ? NS_MAX : FOE_ROUTE_NS;
   dim3 grid(ceil_div(T_, 16 * WPB), C / G);
-  FOE_LAUNCH((route_stream_kernel<NT, FOE_ROUTE_NS, WPB>), grid, dim3(WPB * kWave), 0, s,
+  FOE_LAUNCH((route_stream_kernel<NT, NS, WPB>), grid, dim3(WPB * kWave), 0, s,
              reinterpret_cast<const bf16*>(x), reinterpret_cast<const bf16*>(w), bias, T_, d,
              E, G, k, gating, idx, wt, counts);
   return hipGetLastError();
