@@ -66,23 +66,29 @@ __device__ __forceinline__ void row_softmax_norm(const float (&g)[NT], int col, 
   z = sm;
 }
 
-// Top-k of every group and the routing weights of one token whose G*E
+// Top-k of groups h0 .. h1-1 and the routing weights of one token whose G*E
 // scores sit in a 16-lane row (column nt*16 + col in g[nt], bias included).
-// sel_e / sel_v: this row's k-slot scratch in LDS (a wave's LDS operations
-// complete in order, so the row reads back what its lane col == 0 wrote).
-// Group h writes topk_*[(h*T + tok)*k + s]; with `hist` (LDS, [G*E]) every
-// selected id is also counted there.
+// After each arg-max round every lane of the row holds the selection, so the
+// softmax normaliser is summed as the selections come (slot order), and lane
+// col keeps slot col's id and score for the write (k <= 16).  For k > 16 the
+// slots go through sel_e / sel_v, this row's scratch in LDS (a wave's LDS
+// operations complete in order, so the row reads back what its lane col == 0
+// wrote).  Group h writes topk_*[(h*T + tok)*k + s]; with `hist` (LDS,
+// [G*E]) every selected id is also counted there.
 template <int NT>
-__device__ __forceinline__ void select_token(const float (&g)[NT], int col, int E, int G, int k,
-                                             int gating, int tok, int T_, int* sel_e,
-                                             float* sel_v, int32_t* __restrict__ topk_idx,
+__device__ __forceinline__ void select_token(const float (&g)[NT], int col, int E, int G, int h0,
+                                             int h1, int k, int gating, int tok, int T_,
+                                             int* sel_e, float* sel_v,
+                                             int32_t* __restrict__ topk_idx,
                                              float* __restrict__ topk_w, int* hist) {
   const int Et = G * E;
+  const bool global = gating == FOE_GATE_GLOBAL;
   // global gating: softmax over all G*E scores of the token, not
   // renormalised over the selection
   float gm = 0.f, gz = 1.f;
-  if (gating == FOE_GATE_GLOBAL) row_softmax_norm<NT>(g, col, Et, gm, gz);
-  for (int h = 0; h < G; ++h) {
+  if (global) row_softmax_norm<NT>(g, col, Et, gm, gz);
+  const bool in_regs = k <= 16;
+  for (int h = h0; h < h1; ++h) {
     // bit nt: column nt*16 + col outside group h or already selected
     unsigned taken = 0;
 #pragma unroll
@@ -90,6 +96,9 @@ __device__ __forceinline__ void select_token(const float (&g)[NT], int col, int 
       const int e = nt * 16 + col;
       if (e < h * E || e >= (h + 1) * E) taken |= 1u << nt;
     }
+    float m = gm, z = global ? gz : 0.f;
+    int my_e = -1;
+    float my_v = 0.f;
     for (int s = 0; s < k; ++s) {
       float bv = -__builtin_inff();
       int be = 0x7fffffff;
@@ -103,25 +112,31 @@ __device__ __forceinline__ void select_token(const float (&g)[NT], int col, int 
       argmax_step<2>(bv, be);
       argmax_step<1>(bv, be);
       if (be != 0x7fffffff && (be & 15) == col) taken |= 1u << (be >> 4);
-      if (col == 0) {
-        sel_e[s] = (be == 0x7fffffff) ? -1 : be - h * E;
+      const int id = (be == 0x7fffffff) ? -1 : be - h * E;
+      if (!global) {
+        if (s == 0) m = bv;
+        z += __expf(bv - m);
+      }
+      if (in_regs) {
+        if (s == col) {
+          my_e = id;
+          my_v = bv;
+        }
+      } else if (col == 0) {
+        sel_e[s] = id;
         sel_v[s] = bv;
       }
     }
-    // softmax over the selected scores; lane col writes slots col, col+16, ...
+    // weights: slot s = exp(score_s - m) / z; lane col writes slots col,
+    // col+16, ...
     if (tok < T_) {
-      float m = gm, z = gz;
-      if (gating != FOE_GATE_GLOBAL) {
-        m = sel_v[0];
-        z = 0.f;
-        for (int s = 0; s < k; ++s) z += expf(sel_v[s] - m);
-      }
-      const float inv = 1.0f / z;
+      const float inv = __builtin_amdgcn_rcpf(z);
       const size_t o = ((size_t)h * T_ + tok) * k;
       for (int s = col; s < k; s += 16) {
-        const int id = sel_e[s];
+        const int id = in_regs ? my_e : sel_e[s];
+        const float v = in_regs ? my_v : sel_v[s];
         topk_idx[o + s] = id;
-        topk_w[o + s] = expf(sel_v[s] - m) * inv;
+        topk_w[o + s] = __expf(v - m) * inv;
         if (hist != nullptr && id >= 0) atomicAdd(&hist[h * E + id], 1);
       }
     }
@@ -236,6 +251,10 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
                                                         int32_t* __restrict__ zcnt, int zn,
                                                         int32_t* __restrict__ counts) {
   constexpr int UPW = (4 * TG + NW - 1) / NW;  // units per wave
+  // waves beyond the 4*TG units share the units' groups: wave w takes unit
+  // w % (4*TG) and part w / (4*TG) of its G groups
+  constexpr int PARTS = NW > 4 * TG ? NW / (4 * TG) : 1;
+  static_assert(PARTS == 1 || NW % (4 * TG) == 0, "whole parts");
   extern __shared__ __align__(16) unsigned char smem[];
   // expert counts (with `counts`): G*E ints after the partial-score and
   // selection area (the launch sizes the dynamic LDS for both)
@@ -278,9 +297,10 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
   // scores of this wave's units: sum of the NW partials in wave order, + bias
   const int col = lane & 15;
   float gl[UPW][NT];
+  const int my_unit = PARTS > 1 ? wave % (4 * TG) : wave, gpart = PARTS > 1 ? wave / (4 * TG) : 0;
 #pragma unroll
   for (int u = 0; u < UPW; ++u) {
-    const int unit = wave + u * NW;
+    const int unit = my_unit + u * NW;
     const int g = (unit >> 2) < TG ? (unit >> 2) : 0, i = unit & 3;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -300,13 +320,14 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
   int* sel_e = reinterpret_cast<int*>(smem) + wave * 8 * k;
   float* sel_v = reinterpret_cast<float*>(sel_e + 4 * k);
   const int row = lane >> 4;
+  const int h0 = gpart * G / PARTS, h1 = (gpart + 1) * G / PARTS;
 #pragma unroll
   for (int u = 0; u < UPW; ++u) {
-    const int unit = wave + u * NW;
+    const int unit = my_unit + u * NW;
     if (unit >= 4 * TG) break;
     const int tok = t0 + (unit >> 2) * 16 + 4 * row + (unit & 3);
-    select_token<NT>(gl[u], col, E, G, k, gating, tok, T_, sel_e + row * k, sel_v + row * k,
-                     topk_idx, topk_w, counts != nullptr ? hist : nullptr);
+    select_token<NT>(gl[u], col, E, G, h0, h1, k, gating, tok, T_, sel_e + row * k,
+                     sel_v + row * k, topk_idx, topk_w, counts != nullptr ? hist : nullptr);
   }
   if (counts != nullptr) {
     __syncthreads();
@@ -428,7 +449,7 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
       const int e = nt * 16 + col;
       gl[nt] = acc[nt][i] + ((bias != nullptr && e < Et) ? bias[e] : 0.f);
     }
-    select_token<NT>(gl, col, E, G, k, gating, t0 + 4 * row + i, T_, sel_e, sel_v, topk_idx,
+    select_token<NT>(gl, col, E, G, 0, G, k, gating, t0 + 4 * row + i, T_, sel_e, sel_v, topk_idx,
                      topk_w, counts != nullptr ? hist : nullptr);
   }
   if (counts != nullptr) {
