@@ -501,31 +501,41 @@ __device__ __forceinline__ void gemm_tile(unsigned char* smem, const GemmArgs& g
     constexpr int NM = C::NB * C::SM * C::SN;  // MFMAs per k16 step
     constexpr int NR = C::SM + C::NB * C::SN;  // fragment reads per k16 step
     constexpr int NT = NM > NR ? NM : NR;  // slots of a k16 step
+    // Valid 32-row sub-tiles of this wave's WTM rows: a partly filled tile
+    // (an expert's last rows) skips the MFMAs and A fragment reads of the
+    // sub-tiles past row_end (a variant of the loop; full tiles run without
+    // the checks).
+    const int smv = min(max((row_end - row0 - wm * C::WTM + 31) / 32, 0), C::SM);
+    const bool partial_tile = __builtin_amdgcn_readfirstlane(row_end - row0) < BM;
     // One k16 step in a fixed order: MFMA t of fragment slot `slot`, then
     // fragment read t of (rbuf, rks) into the other slot (rks >= 0), then (in
     // an issuing wave) the DMA instructions [q0, q1) of stage dkt (buffer
-    // dbuf) spread evenly over the MFMAs.
-    auto kstep = [&](auto producer, int slot, int rbuf, int rks, int dkt, int dbuf, int q0,
+    // dbuf) spread evenly over the MFMAs.  mode: bit 0 issuing wave, bit 1
+    // partly filled tile.
+    auto kstep = [&](auto mode, int slot, int rbuf, int rks, int dkt, int dbuf, int q0,
                      int q1) {
+      constexpr bool producer = decltype(mode)::value & 1, part = decltype(mode)::value & 2;
       const unsigned char* sa = smem + rbuf * C::STAGE;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         if (t < NM) {
           const int b = t / (C::SN * C::SM), j = (t / C::SM) % C::SN, i = t % C::SM;
-          acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[slot][b][j], xa[slot][i],
-                                                                 acc[b][i][j], 0, 0, 0);
+          if (!part || i < smv)
+            acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[slot][b][j], xa[slot][i],
+                                                                   acc[b][i][j], 0, 0, 0);
         }
         if (rks >= 0 && t < NR) {
           if (t < C::SM) {
-            xa[slot ^ 1][t] =
-                *reinterpret_cast<const bf16x8*>(sa + a_row + xo[rks] + t * 32 * C::RB);
+            if (!part || t < smv)
+              xa[slot ^ 1][t] =
+                  *reinterpret_cast<const bf16x8*>(sa + a_row + xo[rks] + t * 32 * C::RB);
           } else {
             const int u = t - C::SM, ub = u / C::SN, uj = u % C::SN;
             wf[slot ^ 1][ub][uj] = *reinterpret_cast<const bf16x8*>(
                 sa + b_row + xo[rks] + ub * C::B_BYTES + uj * 32 * C::RB);
           }
         }
-        if constexpr (decltype(producer)::value) {
+        if constexpr (producer) {
 #pragma unroll
           for (int q = q0; q < q1; ++q)
             if ((q - q0) * NT / (q1 - q0) == t) issue_one(dkt, dbuf, q);
@@ -559,21 +569,21 @@ __device__ __forceinline__ void gemm_tile(unsigned char* smem, const GemmArgs& g
     constexpr int VM_AT_BARRIER = NST == 2 ? 0 : (NST - 3) * NLD + BEFORE;
     static_assert(VM_AT_BARRIER <= 63, "vmcnt range");
     auto qof = [&](int st) { return st >= DS ? NLD : QE + st * (NLD - QE) / DS; };
-    auto iteration = [&](auto producer, int kt, int b) {
+    auto iteration = [&](auto mode, int kt, int b) {
       const int dkt = kt + NST - 1, dbuf = (b + NST - 1) % NST;
 #pragma unroll
       for (int st = 0; st + 1 < KS; ++st)
-        kstep(producer, st & 1, b, st + 1, dkt, dbuf, qof(st), qof(st + 1));
+        kstep(mode, st & 1, b, st + 1, dkt, dbuf, qof(st), qof(st + 1));
       vm_barrier<VM_AT_BARRIER>();
       if constexpr (EARLY)  // stage kt+2 into the buffer of stage kt
-        kstep(producer, (KS - 1) & 1, (b + 1) % NST, 0, kt + 2, b, 0, QE);
+        kstep(mode, (KS - 1) & 1, (b + 1) % NST, 0, kt + 2, b, 0, QE);
       else
-        kstep(producer, (KS - 1) & 1, (b + 1) % NST, 0, dkt, dbuf, qof(KS - 1), qof(KS));
+        kstep(mode, (KS - 1) & 1, (b + 1) % NST, 0, dkt, dbuf, qof(KS - 1), qof(KS));
     };
     // the K loop, specialised for issuing and non-issuing waves (both meet
     // the same barriers)
-    auto k_loop = [&](auto producer) {
-      if constexpr (decltype(producer)::value) {
+    auto k_loop = [&](auto mode) {
+      if constexpr (decltype(mode)::value & 1) {
 #pragma unroll
         for (int st = 0; st < NST - 1; ++st)
 #pragma unroll
@@ -594,15 +604,22 @@ __device__ __forceinline__ void gemm_tile(unsigned char* smem, const GemmArgs& g
       fload(0, 0, 0);
       for (int kt = 0; kt < nk; kt += NST) {
 #pragma unroll
-        for (int u = 0; u < NST; ++u) iteration(producer, kt + u, u);
+        for (int u = 0; u < NST; ++u) iteration(mode, kt + u, u);
       }
       // the last DMAs (zeros past K) land before the buffers are reused
       vm_barrier<0>();
     };
-    if (wave_u < C::NP)
-      k_loop(std::true_type{});
-    else
-      k_loop(std::false_type{});
+    if (!partial_tile) {
+      if (wave_u < C::NP)
+        k_loop(std::integral_constant<int, 1>{});
+      else
+        k_loop(std::integral_constant<int, 0>{});
+    } else {
+      if (wave_u < C::NP)
+        k_loop(std::integral_constant<int, 3>{});
+      else
+        k_loop(std::integral_constant<int, 2>{});
+    }
 
     // Thread indices of the epilogue, taken afresh: address arithmetic on
     // the ones above would be hoisted before the K loop and kept live through
