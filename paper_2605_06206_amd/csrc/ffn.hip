@@ -895,6 +895,11 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
 // zeroed before the launch (by the index pass).
 constexpr int kReadyPollLimit = 1 << 20;  // about a second of polling
 
+// M-tiles per group of the fused FFN's tile order (a group's gate/up tiles
+// are walked N-tile by N-tile)
+#ifndef FOE_FUSED_GM
+#define FOE_FUSED_GM 4
+#endif
 // per-XCD work lists from this many groups of M-tiles (fewer groups leave the
 // lists unbalanced, and the tail goes to taking items from other lists)
 #ifndef FOE_FUSED_XCD_MIN_GROUPS
@@ -1556,7 +1561,7 @@ hipError_t launch_expert_ffn_fused(int E, int d, int F, int rows, const void* A,
   if (rows == 0) return hipSuccess;
   static const int cus = device_cus();
   ProfileScope ps("ffn_fused", s);
-  FOE_LAUNCH((ffn_fused_dma<256, 128, 2, 4, 64, 2, 4, 4>), dim3(cus),
+  FOE_LAUNCH((ffn_fused_dma<256, 128, 2, 4, 64, 2, 4, FOE_FUSED_GM>), dim3(cus),
              dim3(8 * kWave), 0, s,
              static_cast<const bf16*>(A), gather, kdiv, a_rows, offsets, E, rows,
              static_cast<const bf16*>(w_gate), static_cast<const bf16*>(w_up),
