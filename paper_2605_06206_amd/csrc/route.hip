@@ -143,6 +143,88 @@ __device__ __forceinline__ void select_token(const float (&g)[NT], int col, int 
   }
 }
 
+// select_token for NB independent (token, group) entries at once: entry b
+// is the token whose scores are g[b] (register index of the 16-lane rows)
+// and its group hg[b] (-1: none).  k <= 16 (slots in registers).  The NB
+// arg-max chains are independent, so their rotation steps interleave instead
+// of running one after another; each entry's results are those of
+// select_token.
+template <int NT, int NB>
+__device__ __forceinline__ void select_batch(const float (&g)[NB][NT], const int (&hg)[NB],
+                                             const int (&tok)[NB], int col, int E, int G, int k,
+                                             int gating, int T_, int32_t* __restrict__ topk_idx,
+                                             float* __restrict__ topk_w, int* hist) {
+  const bool global = gating == FOE_GATE_GLOBAL;
+  unsigned taken[NB];
+  float m[NB], z[NB], my_v[NB];
+  int my_e[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    // bit nt: column nt*16 + col outside the entry's group or already taken
+    taken[b] = 0;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int e = nt * 16 + col;
+      if (hg[b] < 0 || e < hg[b] * E || e >= (hg[b] + 1) * E) taken[b] |= 1u << nt;
+    }
+    m[b] = 0.f;
+    z[b] = 1.f;
+    // global gating: softmax over all G*E scores of the token, not
+    // renormalised over the selection
+    if (global) row_softmax_norm<NT>(g[b], col, G * E, m[b], z[b]);
+    else z[b] = 0.f;
+    my_e[b] = -1;
+    my_v[b] = 0.f;
+  }
+  for (int s = 0; s < k; ++s) {
+    float bv[NB];
+    int be[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      bv[b] = -__builtin_inff();
+      be[b] = 0x7fffffff;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int e = nt * 16 + col;
+        if (!((taken[b] >> nt) & 1u) && beats(g[b][nt], e, bv[b], be[b])) {
+          bv[b] = g[b][nt];
+          be[b] = e;
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b) argmax_step<8>(bv[b], be[b]);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) argmax_step<4>(bv[b], be[b]);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) argmax_step<2>(bv[b], be[b]);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) argmax_step<1>(bv[b], be[b]);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      if (be[b] != 0x7fffffff && (be[b] & 15) == col) taken[b] |= 1u << (be[b] >> 4);
+      if (!global) {
+        if (s == 0) m[b] = bv[b];
+        z[b] += __expf(bv[b] - m[b]);
+      }
+      if (s == col) {
+        my_e[b] = (be[b] == 0x7fffffff) ? -1 : be[b] - hg[b] * E;
+        my_v[b] = bv[b];
+      }
+    }
+  }
+  // weights: slot s = exp(score_s - m) / z, written by lane col = s
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    if (hg[b] >= 0 && tok[b] < T_ && col < k) {
+      const size_t o = ((size_t)hg[b] * T_ + tok[b]) * k + col;
+      topk_idx[o] = my_e[b];
+      topk_w[o] = __expf(my_v[b] - m[b]) * __builtin_amdgcn_rcpf(z[b]);
+      if (hist != nullptr && my_e[b] >= 0) atomicAdd(&hist[hg[b] * E + my_e[b]], 1);
+    }
+  }
+}
+
 // Per-workgroup expert counts (the dispatch histogram, folded in): counts
 // [C][gridDim.x][E] of the workgroup's tokens, cluster = blockIdx.y * G + h.
 __device__ __forceinline__ void write_counts(const int* hist, int G, int E,
@@ -326,8 +408,25 @@ __global__ __launch_bounds__(NW * 64) void route_kernel(const T* __restrict__ x,
     const int unit = my_unit + u * NW;
     if (unit >= 4 * TG) break;
     const int tok = t0 + (unit >> 2) * 16 + 4 * row + (unit & 3);
-    select_token<NT>(gl[u], col, E, G, h0, h1, k, gating, tok, T_, sel_e + row * k,
-                     sel_v + row * k, topk_idx, topk_w, counts != nullptr ? hist : nullptr);
+    if (k <= 16 && h1 - h0 > 1) {
+      // the unit's groups four at a time
+      for (int h = h0; h < h1; h += 4) {
+        float g4[4][NT];
+        int hg[4], tk[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          hg[b] = h + b < h1 ? h + b : -1;
+          tk[b] = tok;
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) g4[b][nt] = gl[u][nt];
+        }
+        select_batch<NT, 4>(g4, hg, tk, col, E, G, k, gating, T_, topk_idx, topk_w,
+                            counts != nullptr ? hist : nullptr);
+      }
+    } else {
+      select_token<NT>(gl[u], col, E, G, h0, h1, k, gating, tok, T_, sel_e + row * k,
+                       sel_v + row * k, topk_idx, topk_w, counts != nullptr ? hist : nullptr);
+    }
   }
   if (counts != nullptr) {
     __syncthreads();
@@ -368,6 +467,14 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int t0 = (blockIdx.x * WPB + wave) * 16;  // this wave's tokens
+  // the bias of this lane's score columns, read before the K loop (read after
+  // it, its latency would follow the loop)
+  float bias_r[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int e = nt * 16 + (lane & 15);
+    bias_r[nt] = (bias != nullptr && e < Et) ? bias[e] : 0.f;
+  }
   const uint32_t lds0 = lds_addr(smem);
   const __amdgpu_buffer_rsrc_t xr = make_rsrc_u(x, (uint32_t)T_ * d * 2u);
   const __amdgpu_buffer_rsrc_t wr = make_rsrc_u(w, (uint32_t)Et * d * 2u);
@@ -441,16 +548,25 @@ __global__ __launch_bounds__(WPB * 64) void route_stream_kernel(
   const int col = lane & 15, row = lane >> 4;
   int* sel_e = sel_buf[wave] + row * 2 * k;
   float* sel_v = reinterpret_cast<float*>(sel_e + k);
+  float gl[4][NT];
+  int tok[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    float gl[NT];
+    tok[i] = t0 + 4 * row + i;
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int e = nt * 16 + col;
-      gl[nt] = acc[nt][i] + ((bias != nullptr && e < Et) ? bias[e] : 0.f);
+    for (int nt = 0; nt < NT; ++nt) gl[i][nt] = acc[nt][i] + bias_r[nt];
+  }
+  if (k <= 16) {
+    for (int h = 0; h < G; ++h) {
+      const int hg[4] = {h, h, h, h};
+      select_batch<NT, 4>(gl, hg, tok, col, E, G, k, gating, T_, topk_idx, topk_w,
+                          counts != nullptr ? hist : nullptr);
     }
-    select_token<NT>(gl, col, E, G, 0, G, k, gating, t0 + 4 * row + i, T_, sel_e, sel_v, topk_idx,
-                     topk_w, counts != nullptr ? hist : nullptr);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      select_token<NT>(gl[i], col, E, G, 0, G, k, gating, tok[i], T_, sel_e, sel_v, topk_idx,
+                       topk_w, counts != nullptr ? hist : nullptr);
   }
   if (counts != nullptr) {
     __syncthreads();
