@@ -885,9 +885,10 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
 // wait always ends: every gate/up tile a down tile waits for is the first
 // item of a workgroup of the grid or was taken from the counter, in order,
 // before the down tile, by a workgroup that is running it (or holds it as its
-// next item behind a gate/up tile); gate/up tiles wait on nothing.  (The wait also gives up after a bounded number of polls, so the
-// launch drains whatever happens; a give-up is counted in sync[1].)  No h row
-// is read before it is complete, and with rows of whole 128-byte lines (F a
+// next item behind a gate/up tile); gate/up tiles wait on nothing.  (The
+// wait also gives up after a bounded number of polls, so the launch drains
+// whatever happens; a give-up is counted in the give-up word of sync.)  No h
+// row is read before it is complete, and with rows of whole 128-byte lines (F a
 // multiple of 64, checked by the caller) no line is shared by two M-tiles, so
 // no XCD's L2 can hold a stale copy of an h line (the L2s hold no h lines from
 // earlier launches: each launch starts with them invalidated).
@@ -896,6 +897,11 @@ void grouped_gemm_dma(const bf16* __restrict__ A, const int32_t* __restrict__ ga
 // zeroed before the launch (by the index pass).
 constexpr int kReadyPollLimit = 1 << 20;  // about a second of polling
 
+// waves of the fused FFN that issue the DMA: all 8 (each its share of a
+// stage, ahead of its MFMAs) measured 2-5% faster than one per SIMD
+#ifndef FOE_FUSED_PW
+#define FOE_FUSED_PW 8
+#endif
 // M-tiles per group of the fused FFN's tile order (a group's gate/up tiles
 // are walked N-tile by N-tile)
 #ifndef FOE_FUSED_GM
@@ -1562,7 +1568,7 @@ hipError_t launch_expert_ffn_fused(int E, int d, int F, int rows, const void* A,
   if (rows == 0) return hipSuccess;
   static const int cus = device_cus();
   ProfileScope ps("ffn_fused", s);
-  FOE_LAUNCH((ffn_fused_dma<256, 128, 2, 4, 64, 2, 4, FOE_FUSED_GM>), dim3(cus),
+  FOE_LAUNCH((ffn_fused_dma<256, 128, 2, 4, 64, 2, FOE_FUSED_PW, FOE_FUSED_GM>), dim3(cus),
              dim3(8 * kWave), 0, s,
              static_cast<const bf16*>(A), gather, kdiv, a_rows, offsets, E, rows,
              static_cast<const bf16*>(w_gate), static_cast<const bf16*>(w_up),
