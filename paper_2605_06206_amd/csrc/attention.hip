@@ -28,6 +28,19 @@ constexpr int kKB = 64;   // keys per block of the V^T layout (its zero padding)
 // floor of the running maximum (log2 units): finite, and far below any score
 constexpr float kMFloor = -1.0e30f;
 
+// Attention inner step: fragment reads in flight ahead of the score and P V
+// MFMAs, and vector instructions placed after each P V MFMA; FOE_ATT_SGB 0
+// leaves the order to the compiler.
+#ifndef FOE_ATT_KW
+#define FOE_ATT_KW 4
+#endif
+#ifndef FOE_ATT_VPM
+#define FOE_ATT_VPM 8
+#endif
+#ifndef FOE_ATT_SGB
+#define FOE_ATT_SGB 1
+#endif
+
 // ---- preparation pass ----------------------------------------------------------
 // One workgroup per (64-row block, group).  (1) Rotary embedding of the q and
 // k heads in place: each angle (s / scale) * theta^(-2i/HD) is formed once,
@@ -293,41 +306,57 @@ __global__ __launch_bounds__(NP * NH * 128) __attribute__((amdgpu_waves_per_eu(2
   const int nkb = min((qb + 1) * (kQB / KB), (S + KB - 1) / KB);
   const int niter = (nkb + NP - 1) / NP;  // every part runs the same iterations
   if (part < nkb) issue_k(0);
-  for (int it = 0; it < niter; ++it) {
-    const int kb = NP * it + part;
-    const bool valid = kb < nkb;  // wave-uniform
-    // K of this block and V of the previous one have landed for every wave,
-    // and every wave is done with the previous iteration's stages
-    vm_barrier<0>();
-    if (kb + NP < nkb) issue_k(it + 1);
-    if (valid) issue_v(it);
-    const unsigned char* ks = hs + (it & 1) * KT;
-    const unsigned char* vs = hs + 2 * KT + ((it + 1) & 1) * VT;  // previous block's V
-
+  // One key block of a part, in two stretches of branch-free code (scheduling
+  // regions) with the masking between them, on the blocks that reach the
+  // causal diagonal or the end of the sequence (`masked`, wave-uniform):
+  //   scores S^T = K Q^T, the K fragment reads KW ahead of the MFMAs and the
+  //   first V^T reads behind them;
+  //   O^T += V^T P^T of the previous block, each MFMA followed by one V^T read
+  //   and a share of the softmax of this block (maximum, exponentials,
+  //   packing, row sums), written to fresh registers that become P afterwards,
+  //   so that the vector ALUs work while the MFMAs run.
+  // (The masked and unmasked steps as two compiled copies, one region each,
+  // needed 256 registers at HD = 128 and ran slower.)
+  auto block_step = [&](bool masked, const unsigned char* ks, const unsigned char* vs,
+                        int kbase) {
+    constexpr int NS = NST * NSC;   // score MFMAs, st-major
+    constexpr int NV = NKS * NDT;   // P V MFMAs, u-major
+    constexpr int KW = FOE_ATT_KW;  // K fragment reads in flight
+    constexpr int VW = KW;          // V^T fragment reads in flight
     f32x16 sacc[NSC];
-    if (valid) {
 #pragma unroll
-      for (int t = 0; t < NSC; ++t)
+    for (int t = 0; t < NSC; ++t)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) sacc[t][v] = 0.f;
+      for (int v = 0; v < 16; ++v) sacc[t][v] = 0.f;
+    bf16x8 kf[NS];
+    auto kread = [&](int j) {
+      const int st = j / NSC, t = j % NSC, row = t * 32 + qi;
+      kf[j] = *reinterpret_cast<const bf16x8*>(ks + row * 256 + (((st * 2 + hl) ^ (row & 15)) << 4));
+    };
+    bf16x8 vf[NV];
+    auto vread = [&](int j) {
+      const int u = j / NDT, dt = j % NDT, row = dt * 32 + qi;
+      vf[j] = *reinterpret_cast<const bf16x8*>(vs + row * (KB * 2) +
+                                               (((u * 2 + hl) ^ swz<VC>(row)) << 4));
+    };
 #pragma unroll
-      for (int st = 0; st < NST; ++st)
+    for (int j = 0; j < KW; ++j) kread(j);
 #pragma unroll
-        for (int t = 0; t < NSC; ++t) {
-          const int row = t * 32 + qi;
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
-              ks + row * 256 + (((st * 2 + hl) ^ (row & 15)) << 4));
-          sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st], sacc[t], 0, 0, 0);
-        }
+    for (int j = 0; j < NS; ++j) {
+      if (j + KW < NS) kread(j + KW);
+      else vread(j + KW - NS);
+      sacc[j % NSC] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[j], qf[j / NSC], sacc[j % NSC], 0, 0, 0);
     }
-    if (resc) {
+#if FOE_ATT_SGB
 #pragma unroll
-      for (int t = 0; t < NDT; ++t)
+    for (int j = 0; j < KW; ++j) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
 #pragma unroll
-        for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
+    for (int j = 0; j < NS; ++j) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
-    const int kbase = kb * KB;
-    if (valid && (kbase + KB - 1 > q0 || kbase + KB > S)) {  // wave-uniform
+#endif
+    if (masked) {
 #pragma unroll
       for (int t = 0; t < NSC; ++t)
 #pragma unroll
@@ -336,48 +365,90 @@ __global__ __launch_bounds__(NP * NH * 128) __attribute__((amdgpu_waves_per_eu(2
           if (key > q || key >= S) sacc[t][v] = -__builtin_inff();
         }
     }
-
-    // O^T += V^T P^T for the previous block (zeros at the first iteration)
-    pv(oacc, pf, vs);
-
-    if (valid) {
-      // softmax of this block
-      float mx = sacc[0][0];
+    // softmax of this block: maximum over the row's keys (the two lane halves
+    // hold the two key halves of the same queries)
+    float mx = sacc[0][0];
 #pragma unroll
-      for (int t = 0; t < NSC; ++t)
+    for (int t = 0; t < NSC; ++t)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[t][v]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mxs = mx * c_log2;
-      // a row with a visible key in the block has a finite mxs, far above
-      // the floor, so the first such block always moves m; a row without one
-      // (mxs = -inf) keeps m and gets p = 0
-      const bool need = mxs > m_run + 8.f;
-      const float m_new = need ? mxs : m_run;
-      alpha = need ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
-      m_run = m_new;
-      resc = __builtin_amdgcn_ballot_w64(need) != 0;
-      float ps = 0.f;
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[t][v]);
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                       false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    }
+    const float mxs = mx * c_log2;
+    // a row with a visible key in the block has a finite mxs, far above the
+    // floor, so the first such block always moves m; a row without one
+    // (mxs = -inf) keeps m and gets p = 0
+    const bool need = mxs > m_run + 8.f;
+    const float m_new = need ? mxs : m_run;
+    const float a_new = need ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
+    bf16x8 pn[NKS];
+    float ps = 0.f;
 #pragma unroll
-      for (int u = 0; u < NKS; ++u) {
-        bf16x8 p8;
+    for (int u = 0; u < NKS; ++u) {
+      // P V MFMAs of key step u of the previous block
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          p8[e] = (bf16)__builtin_amdgcn_exp2f(
-              fmaf(sacc[u >> 1][(u & 1) * 8 + e], c_log2, -m_run));
-        pf[u] = p8;
-#pragma unroll
-        for (int e = 0; e < 8; e += 2)
-          ps = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p8[e], p8[e + 1]},
-                                               bf16x2{(bf16)1.f, (bf16)1.f}, ps, false);
+      for (int dt = 0; dt < NDT; ++dt) {
+        const int j = u * NDT + dt;
+        if (j + VW < NV) vread(j + VW);
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[j], pf[u], oacc[dt], 0, 0, 0);
       }
-      l_run = l_run * alpha + ps;
-    } else {
+      bf16x8 p8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        p8[e] = (bf16)__builtin_amdgcn_exp2f(fmaf(sacc[u >> 1][(u & 1) * 8 + e], c_log2, -m_new));
+      pn[u] = p8;
+#pragma unroll
+      for (int e = 0; e < 8; e += 2)
+        ps = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p8[e], p8[e + 1]},
+                                             bf16x2{(bf16)1.f, (bf16)1.f}, ps, false);
+    }
+#pragma unroll
+    for (int u = 0; u < NKS; ++u) pf[u] = pn[u];
+#if FOE_ATT_SGB
+    constexpr int VPM = FOE_ATT_VPM;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (j + VW < NV) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, VPM, 0);  // VALU
+    }
+#endif
+    resc = __builtin_amdgcn_ballot_w64(need) != 0;
+    alpha = a_new;
+    m_run = m_new;
+    l_run = l_run * a_new + ps;
+  };
+
+  for (int it = 0; it < niter; ++it) {
+    const int kb = NP * it + part;
+    // K of this block and V of the previous one have landed for every wave,
+    // and every wave is done with the previous iteration's stages
+    vm_barrier<0>();
+    if (kb + NP < nkb) issue_k(it + 1);
+    if (kb < nkb) issue_v(it);
+    const unsigned char* ks = hs + (it & 1) * KT;
+    const unsigned char* vs = hs + 2 * KT + ((it + 1) & 1) * VT;  // previous block's V
+    // the rescale owed by the previous block's softmax, before its P V
+    if (resc) {
+#pragma unroll
+      for (int t = 0; t < NDT; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
+    }
+    if (kb >= nkb) {  // wave-uniform: this part has no block left
+      pv(oacc, pf, vs);
       resc = false;
       alpha = 1.f;
 #pragma unroll
       for (int u = 0; u < NKS; ++u) pf[u] = bf16x8{};
+      continue;
     }
+    const int kbase = kb * KB;
+    const bool edge = kbase + KB - 1 > q0 || kbase + KB > S;  // wave-uniform
+    block_step(edge, ks, vs, kbase);
   }
   // the last block's P V (P = 0 if the part's last iteration had no block)
   vm_barrier<0>();
