@@ -323,6 +323,7 @@ __global__ __launch_bounds__(NP * NH * 128) __attribute__((amdgpu_waves_per_eu(2
     constexpr int NV = NKS * NDT;   // P V MFMAs, u-major
     constexpr int KW = FOE_ATT_KW;  // K fragment reads in flight
     constexpr int VW = KW;          // V^T fragment reads in flight
+    static_assert(KW <= NS && VW <= NV, "reads in flight within one step");
     f32x16 sacc[NSC];
 #pragma unroll
     for (int t = 0; t < NSC; ++t)
