@@ -419,10 +419,12 @@ __device__ __forceinline__ void gemm_tile(unsigned char* smem, const GemmArgs& g
 
     // Several issuing waves: wave p loads instructions p*NLD .. p*NLD+NLD-1,
     // all inside tile tw starting at its instruction ii0.
-    // With eight issuing waves, waves 0..3 (the older wave of each SIMD)
-    // take the weight shares and waves 4..7 the A rows (measured 1% faster
-    // at the prefill load than the other way round, the same elsewhere;
-    // results identical).  With four or fewer the rotation is the identity.
+    // Share p goes to wave (p + 4) mod NP.  With eight issuing waves, waves
+    // 0..3 (the older wave of each SIMD) take the weight shares and waves
+    // 4..7 the A rows (measured 1% faster at the prefill load than the other
+    // way round, the same elsewhere; results identical).  With four issuing
+    // waves this is the identity; with three (the residual GEMM) each share
+    // moves to the next wave.
 #ifndef FOE_DMA_ROT
 #define FOE_DMA_ROT 4
 #endif
